@@ -1,0 +1,63 @@
+"""Pins of the fp64 GEMM oracle and its error metrics (Sec. II-B, C = A B)."""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import gemm as O
+
+
+def test_decode_matches_bf16_definition():
+    # 1.0 = 0x3F80, -2.0 = 0xC000, 0.5 = 0x3F00, smallest normal 2^-126 = 0x0080
+    bits = np.array([0x3F80, 0xC000, 0x3F00, 0x0080, 0x0000, 0x8000], dtype=np.uint16)
+    assert list(O.decode_bf16(bits)) == [1.0, -2.0, 0.5, 2.0 ** -126, 0.0, -0.0]
+
+
+@pytest.mark.parametrize("M,N,K", [(256, 512, 256), (37, 19, 256), (128, 128, 1), (64, 64, 64)])
+def test_ternary_inputs_match_exact_integer_product(M, N, K):
+    A = W.draw_array(11, M, K, "ternary")
+    B = W.draw_array(12, K, N, "ternary")
+    Ai = O.decode_bf16(A).astype(np.int64)
+    Bi = O.decode_bf16(B).astype(np.int64)
+    C = O.gemm_fp64(A, B)
+    assert np.array_equal(C, (Ai @ Bi).astype(np.float64))
+
+
+def test_identity_b_returns_a():
+    A = W.draw_array(3, 64, 96, "normal", 1.0)
+    I = W.round_to_bf16_bits(np.eye(96, dtype=np.float32))
+    assert np.array_equal(O.gemm_fp64(A, I), O.decode_bf16(A))
+
+
+def test_entries_match_fsum_definition():
+    A = W.draw_array(4, 40, 300, "normal", 1.0)
+    B = W.draw_array(5, 300, 50, "normal", 0.02)
+    C = O.gemm_fp64(A, B)
+    a, b = O.decode_bf16(A), O.decode_bf16(B)
+    rng = np.random.default_rng(0)
+    rows = rng.integers(0, 40, 25)
+    cols = rng.integers(0, 50, 25)
+    ent = O.gemm_entries(A, B, rows, cols)
+    for i, (r, c) in enumerate(zip(rows, cols)):
+        exact = math.fsum(a[r, k] * b[k, c] for k in range(300))
+        assert abs(C[r, c] - exact) <= 1e-12 * (1 + abs(exact))
+        assert abs(ent[i] - exact) <= 1e-12 * (1 + abs(exact))
+
+
+def test_error_metrics_on_known_perturbation():
+    rng = np.random.default_rng(1)
+    ref = rng.standard_normal((30, 20))
+    err = O.errors(ref * (1 + 1e-3), ref)
+    assert math.isclose(err["rel_fro"], 1e-3, rel_tol=1e-9)
+    assert math.isclose(err["max_abs"], 1e-3 * np.abs(ref).max(), rel_tol=1e-9)
+    assert O.within_tolerance(err)
+    bad = ref.copy()
+    bad[3, 4] += 0.5 * np.abs(ref).max()
+    e2 = O.errors(bad, ref)
+    assert e2["max_abs"] > 1e-2 * e2["max_ref"] and not O.within_tolerance(e2)
+
+
+def test_inner_dimension_mismatch_raises():
+    with pytest.raises(ValueError):
+        O.gemm_fp64(np.zeros((2, 3)), np.zeros((4, 2)))
