@@ -1,0 +1,225 @@
+"""Throughput of the CCL GEMM hot path on one MI355X.
+
+Workload (Llama-3.1-70B dense FFN forward, 8192 tokens, bf16, 8 chiplet
+partitions on a 2x4 grid, 4 KB pages): one step is
+    pack X (8192x8192, row-major -> CCL)
+    H = X W_up        (8192x28672x8192, CCL GEMM)
+    Y = H W_down      (8192x8192x28672, CCL GEMM; H is read in the CCL
+                       layout the first GEMM wrote: same block grid)
+    unpack Y (CCL -> row-major)
+The weights are packed into CCL once before timing (load-time packing).
+Inputs are synthetic (seeded, workloads module) and resident in HBM.
+
+Prints one JSON line: value = GEMM TFLOP/s of the whole step, plus the
+roofline of the dominant kernel (the GEMM, timed per launch with HIP events
+on its stream), the remote-HBM-byte model for both GEMMs, and the CPU
+oracle timed on a bounded sample (rank 0, one GPU only).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "CCL bf16 GEMM TFLOP/s (% MFMA peak); remote-HBM-byte reduction vs 4KB interleave"
+PEAK_BF16_TFLOPS = 2516.6        # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense)
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama_fwd_traffic.json")
+GEMM_SRC = os.path.join(ROOT, "paper_2606_11718_amd", "csrc", "kernels", "gemm.hip")
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(launch_flops_unused=None):
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter runs,
+    if they were taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    t = json.load(open(TRAFFIC_FILE))
+    if t.get("kernel_hash") != kernel_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(target_s: float):
+    """The oracle's fp64 GEMM on a row sample of the up-projection GEMM."""
+    import numpy as np
+    import threadpoolctl
+    import workloads as W
+    from oracle import gemm as OG
+
+    wl, g = W.gemm_by_name("llama_up")
+    B = W.draw(wl.tensors[g.b_src])
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+
+    def run(rows):
+        A = W.draw(wl.tensors[g.a_src], rows=slice(0, rows))
+        t0 = time.perf_counter()
+        OG.gemm_fp64(A, B)
+        return time.perf_counter() - t0
+
+    t_cal = run(16)
+    rows = int(max(16, min(g.M, 16 * target_s / max(t_cal, 1e-3))))
+    rows = max(16, (rows // 16) * 16)
+    t = run(rows)
+    flops = 2.0 * rows * g.N * g.K
+    return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"fp64 oracle GEMM of the first {rows} of 8192 rows of X times W_up "
+                      f"(8192x28672), {flops / 1e12:.3f} TFLOP in {t:.2f} s, bf16 decode included"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); the CCL GEMM "
+              "path here has no multi-GPU sharding.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2606_11718_amd import ccl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = W.WORKLOADS["llama_fwd"]
+    _, g_up = W.gemm_by_name("llama_up")
+    _, g_dn = W.gemm_by_name("llama_down")
+    P, G, Gr = 4096, 8, 2
+    plan_up = ccl.ccl_plan(g_up.M, g_up.N, g_up.K, G, Gr, P)
+    plan_dn = ccl.ccl_plan(g_dn.M, g_dn.N, g_dn.K, G, Gr, P)
+    L = {name: ccl.ccl_plan_layout(p, op) for name, p, op in
+         (("X", plan_up, ccl.CCL_A), ("Wup", plan_up, ccl.CCL_B), ("H", plan_up, ccl.CCL_C),
+          ("Hin", plan_dn, ccl.CCL_A), ("Wdn", plan_dn, ccl.CCL_B), ("Y", plan_dn, ccl.CCL_C))}
+    # the up GEMM's C layout is the down GEMM's A layout (same grid over 8192 x 28672)
+    assert L["H"] == L["Hin"]
+
+    def dev_bits(t):
+        return torch.from_numpy(W.draw(wl.tensors[t]).view(np.int16)).to(dev)
+
+    def empty(lay):
+        return torch.empty(lay.total_bytes // 2, dtype=torch.int16, device=dev)
+
+    X = dev_bits("X")
+    Wup_c, Wdn_c = empty(L["Wup"]), empty(L["Wdn"])
+    w = dev_bits("W_up")
+    ccl.ccl_pack(plan_up, ccl.CCL_B, w, g_up.N, 0, Wup_c)
+    torch.cuda.synchronize()
+    del w
+    w = dev_bits("W_down")
+    ccl.ccl_pack(plan_dn, ccl.CCL_B, w, g_dn.N, 0, Wdn_c)
+    torch.cuda.synchronize()
+    del w
+    Xc, Hc, Yc = empty(L["X"]), empty(L["H"]), empty(L["Y"])
+    Y = torch.empty(g_dn.M, g_dn.N, dtype=torch.int16, device=dev)
+
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    marks = []
+
+    def step(timed):
+        e = [ev() for _ in range(5)] if timed else None
+        if timed:
+            e[0].record(stream)
+        ccl.ccl_pack(plan_up, ccl.CCL_A, X, g_up.K, 0, Xc, stream)
+        if timed:
+            e[1].record(stream)
+        ccl.ccl_gemm(plan_up, Xc, Wup_c, Hc, stream)
+        if timed:
+            e[2].record(stream)
+        ccl.ccl_gemm(plan_dn, Hc, Wdn_c, Yc, stream)
+        if timed:
+            e[3].record(stream)
+        ccl.ccl_unpack(plan_dn, ccl.CCL_C, Yc, Y, g_dn.N, stream)
+        if timed:
+            e[4].record(stream)
+            marks.append(e)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0, t1 = ev(), ev()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / args.steps
+    per = {"pack_x": [], "gemm_up": [], "gemm_down": [], "unpack_y": []}
+    for e in marks:
+        per["pack_x"].append(e[0].elapsed_time(e[1]))
+        per["gemm_up"].append(e[1].elapsed_time(e[2]))
+        per["gemm_down"].append(e[2].elapsed_time(e[3]))
+        per["unpack_y"].append(e[3].elapsed_time(e[4]))
+    avg = {k: float(np.mean(v)) for k, v in per.items()}
+
+    gemm_flops = float(g_up.flops)                  # = g_dn.flops
+    step_flops = g_up.flops + g_dn.flops
+    value = step_flops / (ms_step * 1e-3) / 1e12
+    gemm_ms = (avg["gemm_up"] + avg["gemm_down"]) / 2
+    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    traffic = measured_traffic()
+    copy_bytes = 2 * 8192 * 8192 * 2                # read + write of X (or Y)
+
+    remote = {}
+    for name, p, g in (("llama_up", plan_up, g_up), ("llama_down", plan_dn, g_dn)):
+        r = {pl: sum(ccl.ccl_remote_bytes(p, code, 0)["remote"])
+             for pl, code in (("rr_4k", ccl.CCL_PLACE_RR), ("coarse_4k", ccl.CCL_PLACE_COARSE),
+                              ("ccl_4k", ccl.CCL_PLACE_CCL))}
+        r["rr_over_ccl"] = round(r["rr_4k"] / r["ccl_4k"], 4)
+        r["coarse_over_ccl"] = round(r["coarse_4k"] / r["ccl_4k"], 4)
+        remote[name] = r
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama_fwd: Llama-3.1-70B-like FFN forward, X[8192x8192] W_up[8192x28672] "
+                               "then H W_down[28672x8192], 8 XCD partitions on a 2x4 grid, 4 KB pages",
+                   "tokens": 8192, "grid": "2x4", "chiplets": G, "page_bytes": P,
+                   "gemm_tile": list(ccl.ccl_debug_gemm_config(plan_up)[:2])},
+        "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic, "kernel": "gemm_kernel<256,256> (up and down launches)",
+                     "avg_launch_ms": round(gemm_ms, 4)},
+        "kernels_ms": {k: round(v, 4) for k, v in avg.items()},
+        "copy_roofline": {"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                          "pack_x": round(copy_bytes / (avg["pack_x"] * 1e-3) / 1e9, 1),
+                          "unpack_y": round(copy_bytes / (avg["unpack_y"] * 1e-3) / 1e9, 1)},
+        "remote_bytes": remote,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

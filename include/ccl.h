@@ -1,0 +1,191 @@
+/*
+ * ccl.h - GEMM on operands stored in Chiplet-Contiguous Layout (CCL),
+ *         for AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Making Locality-aware GEMM Compatible with Page-Granularity
+ * Placement on Chiplet GPUs" (Chung, Ju, Kim).
+ *   - C = A B with A (M x K), B (K x N), C (M x N), Sec. II-B.
+ *   - Each chiplet's operand share is one contiguous, page-aligned strip:
+ *     Sec. III-B, Eq. 1-3 (CCL index g*K*w + k*w + n'), Sec. III-C.
+ *   - Output tiles run on the chiplet that owns them (Sec. III-A) and the
+ *     GEMM arithmetic itself is unchanged (Sec. III-C).
+ *   - Remote-HBM traffic under 4 KB round-robin interleave, coarse
+ *     locality-aware placement and CCL, Sec. IV-A.
+ *
+ * Conventions for every call:
+ *   - Element type is bfloat16 (2 bytes) for A, B and C (Sec. IV-A: BF16
+ *     GEMMs). Device buffers are passed as plain device pointers.
+ *   - Logical operands are row-major: A is M x K, B is K x N, C is M x N.
+ *   - The caller owns every buffer and the stream. The library allocates no
+ *     device memory. A plan is owned by the caller from ccl_plan() until
+ *     ccl_plan_destroy(); it is immutable, so calls on one plan may run from
+ *     several host threads.
+ *   - Device calls (ccl_pack, ccl_unpack, ccl_gemm, ccl_debug_dispatch) are
+ *     asynchronous on `stream` (a hipStream_t passed as void*; NULL is the
+ *     null stream). ccl_plan*, ccl_remote_bytes and ccl_debug_tile_of_wg are
+ *     host-only and need no GPU.
+ *   - Every call returns a ccl_status. On any error nothing is written and
+ *     nothing is launched; ccl_last_error() gives a per-thread message.
+ *
+ * CCL layout of an operand X (R x Cc) under a Gr x Gc grid (the same grid
+ * is laid over each operand's own rows and columns: A is split along K by
+ * Gc, B along K by Gr):
+ *   hr = R / Gr, wc = Cc / Gc, block b(r, c) = (r / hr) * Gc + c / wc,
+ *   strip bytes S = ceil(hr * wc * 2 / page) * page,
+ *   byte offset(r, c) = b * S + ((r % hr) * wc + c % wc) * 2.
+ * Block b lives on chiplet b. With Gr = 1 and no padding this is Eq. 3.
+ * Padding bytes at the end of each strip are never read or written.
+ */
+#ifndef CCL_H_
+#define CCL_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ccl_plan_s* ccl_plan_t;
+
+typedef enum {
+  CCL_OK = 0,
+  CCL_ERR_INVALID_ARG = 1,          /* bad size, grid, page, operand, null pointer */
+  CCL_ERR_UNALIGNED_PARTITION = 2,  /* partitions not multiples of the 128x128 tile */
+  CCL_ERR_UNSUPPORTED = 3,          /* valid plan the GPU path does not run */
+  CCL_ERR_MISALIGNED_POINTER = 4,   /* device pointer / leading dimension alignment */
+  CCL_ERR_HIP = 5                   /* HIP runtime error (launch, device query) */
+} ccl_status;
+
+typedef enum { CCL_A = 0, CCL_B = 1, CCL_C = 2 } ccl_operand;
+
+typedef enum {
+  CCL_PLACE_RR = 0,      /* fixed-size pages to chiplets round-robin (Sec. IV-A) */
+  CCL_PLACE_COARSE = 1,  /* G contiguous page-granular chunks (Sec. IV-A, Coarse LA) */
+  CCL_PLACE_CCL = 2      /* CCL strips, each strip's pages on its chiplet */
+} ccl_placement;
+
+/* Layout of one operand in CCL. All sizes in elements unless named _bytes. */
+typedef struct {
+  int64_t rows, cols;            /* logical operand shape */
+  int64_t grid_r, grid_c;        /* block grid over (rows, cols) */
+  int64_t block_rows, block_cols;
+  int64_t strip_bytes;           /* block_rows * block_cols * 2 */
+  int64_t strip_stride_bytes;    /* strip_bytes rounded up to the page */
+  int64_t total_bytes;           /* grid_r * grid_c * strip_stride_bytes: buffer size */
+} ccl_layout;
+
+#define CCL_MAX_CHIPLETS 64
+
+/* Remote-byte record (Sec. IV-A metric, no cache): every 128x128 output
+ * tile runs on its owner chiplet, reads its full A row panel and B column
+ * panel and writes its C tile; an access is remote iff its page is on
+ * another chiplet. Index [0]=A, [1]=B, [2]=C. */
+typedef struct {
+  uint64_t accessed[3];          /* bytes read (A, B) or written (C) */
+  uint64_t remote[3];            /* of which remote */
+  uint64_t floor_bytes;          /* lower bound of remote bytes for any layout */
+  uint64_t footprint[3];         /* stored bytes of each operand, padding included */
+  uint64_t remote_per_chiplet[CCL_MAX_CHIPLETS];  /* charged to the requesting owner */
+  int32_t chiplets;
+} ccl_traffic;
+
+/*
+ * Create a plan for C = A B over `chiplets` chiplets (1..64) on a
+ * grid_rows x (chiplets / grid_rows) output-partition grid, with strips
+ * padded to `page_bytes` (power of two, >= 128). grid_rows = 0 chooses the
+ * grid per GEMM (Sec. IV-A "Baselines": CCL picks coarse or fine
+ * partitioning per GEMM): the tile-aligned grid with the fewest CCL remote
+ * bytes, then the one whose shared operands replicate fewer bytes, then the
+ * smaller grid_rows.
+ * Errors: CCL_ERR_INVALID_ARG (non-positive size, chiplets out of range,
+ * grid_rows not dividing chiplets, bad page, out == NULL, size overflow);
+ * CCL_ERR_UNALIGNED_PARTITION (M % (Gr*128), N % (Gc*128), K % Gr or
+ * K % Gc not zero, or no aligned grid for grid_rows = 0).
+ */
+ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
+                    int64_t page_bytes, ccl_plan_t* out);
+
+/* Release a plan. NULL is accepted. */
+ccl_status ccl_plan_destroy(ccl_plan_t plan);
+
+/* Grid the plan uses (after automatic choice). */
+ccl_status ccl_plan_grid(ccl_plan_t plan, int* grid_rows, int* grid_cols);
+
+/* Layout of operand `op`: buffer size and strip geometry (Sec. III-B). */
+ccl_status ccl_plan_layout(ccl_plan_t plan, ccl_operand op, ccl_layout* out);
+
+/*
+ * Pack a stored operand into CCL (Sec. III-C: weights packed at load time,
+ * activations repacked). src_trans = 0: src is the row-major operand
+ * (rows x cols, leading dimension ld >= cols elements). src_trans = 1: src
+ * holds the transpose (cols x rows, ld >= rows), e.g. H for A = H^T.
+ * dst_ccl has ccl_plan_layout().total_bytes bytes; padding is not written.
+ * Errors: CCL_ERR_INVALID_ARG (null pointer, op not A/B/C, ld too small,
+ * src_trans on C); CCL_ERR_HIP.
+ */
+ccl_status ccl_pack(ccl_plan_t plan, ccl_operand op, const void* src, int64_t ld,
+                    int src_trans, void* dst_ccl, void* stream);
+
+/*
+ * Inverse of ccl_pack with src_trans = 0: CCL buffer -> row-major operand
+ * (rows x cols, leading dimension ld >= cols). Columns beyond cols in each
+ * dst row are not written. Errors as ccl_pack.
+ */
+ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void* dst,
+                      int64_t ld, void* stream);
+
+/*
+ * C_ccl = A_ccl B_ccl, all three in the plan's CCL layouts: bf16 inputs,
+ * fp32 accumulation on the matrix cores, bf16 output rounded to nearest
+ * even (Sec. II-B, III-C). Each XCD computes exactly the output tiles of
+ * the partition its chiplet owns (chiplet c <-> XCDs c*8/G .. c*8/G+8/G-1),
+ * so chiplets must divide 8.
+ * Errors: CCL_ERR_INVALID_ARG (null pointer); CCL_ERR_MISALIGNED_POINTER
+ * (pointer not 16-byte aligned); CCL_ERR_UNSUPPORTED (chiplets not dividing
+ * 8, K / Gc or K / Gr not a multiple of 64, device not gfx950);
+ * CCL_ERR_HIP.
+ */
+ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
+                    void* stream);
+
+/*
+ * Remote-byte record of the plan's GEMM under `placement` (Sec. IV-A).
+ * stored_trans_mask bit 0: A is stored transposed; bit 1: B is stored
+ * transposed (affects RR and COARSE only: they place pages of the stored
+ * tensor). Host-only, synchronous. Errors: CCL_ERR_INVALID_ARG.
+ */
+ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+                            ccl_traffic* out);
+
+/* Static name of a status code. */
+const char* ccl_status_string(ccl_status status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* ccl_last_error(void);
+
+/*
+ * Test hook: which XCD runs workgroup `wg` of ccl_gemm's launch (dispatch
+ * is round-robin: wg mod 8) and which kernel output tile (tile_m, tile_n)
+ * it computes, in units of the kernel tile (tile_rows x tile_cols, see
+ * ccl_debug_gemm_config); -1 for both when the workgroup has no tile.
+ */
+ccl_status ccl_debug_tile_of_wg(ccl_plan_t plan, int64_t wg, int* xcd, int64_t* tile_m,
+                                int64_t* tile_n);
+
+/* Test hook: the GEMM kernel tile and launch size the plan uses. */
+ccl_status ccl_debug_gemm_config(ccl_plan_t plan, int* tile_rows, int* tile_cols,
+                                 int64_t* workgroups);
+
+/*
+ * Test hook: launch a kernel with ccl_gemm's grid in which every workgroup
+ * records, at out[4*wg .. 4*wg+3], the hardware XCD id it ran on, its tile
+ * (tile_m, tile_n; -1 if none) and the chiplet owning that tile. `out` is a
+ * device buffer of 4 * workgroups int32. Errors as ccl_gemm.
+ */
+ccl_status ccl_debug_dispatch(ccl_plan_t plan, int32_t* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CCL_H_ */

@@ -1,0 +1,228 @@
+// C ABI of the CCL library (declarations and contracts: include/ccl.h).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+
+#include "../../include/ccl.h"
+#include "host/plan.hpp"
+#include "kernels/kernels.hpp"
+
+struct ccl_plan_s {
+  ccl::Plan plan;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ccl_status fail(ccl_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+ccl_status ok() {
+  g_last_error.clear();
+  return CCL_OK;
+}
+
+ccl_status from(ccl::Status s, const std::string& msg) {
+  return s == ccl::Status::OK ? ok() : fail(static_cast<ccl_status>(s), msg);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// gfx950 check, once per device.
+constexpr int kMaxDevices = 64;
+std::once_flag g_dev_once[kMaxDevices];
+bool g_dev_ok[kMaxDevices];
+
+ccl_status check_device() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CCL_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(CCL_ERR_UNSUPPORTED, "device index out of range");
+  std::call_once(g_dev_once[dev], [dev] {
+    hipDeviceProp_t prop;
+    g_dev_ok[dev] = hipGetDeviceProperties(&prop, dev) == hipSuccess &&
+                    std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  });
+  if (!g_dev_ok[dev]) return fail(CCL_ERR_UNSUPPORTED, "the GPU kernels are built for gfx950 only");
+  return CCL_OK;
+}
+
+ccl_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(CCL_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return ok();
+}
+
+bool valid_op(ccl_operand op) { return op == CCL_A || op == CCL_B || op == CCL_C; }
+
+// CCL addressing of the GEMM operands (elements).
+void ccl_addressing(const ccl::Plan& p, ccl::OperandAddr* a, ccl::OperandAddr* b,
+                    ccl::OperandAddr* c) {
+  const int64_t sa = p.lay[ccl::OP_A].strip_stride_bytes / 2;
+  const int64_t sb = p.lay[ccl::OP_B].strip_stride_bytes / 2;
+  const int64_t sc = p.lay[ccl::OP_C].strip_stride_bytes / 2;
+  // A block (pr, kc) = pr*Gc + kc; B block (kr, pc) = kr*Gc + pc; C block (pr, pc).
+  *a = {p.Gc * sa, sa, (int32_t)(p.K / p.Gc), (int32_t)(p.K / p.Gc)};
+  *b = {sb, p.Gc * sb, (int32_t)(p.N / p.Gc), (int32_t)(p.K / p.Gr)};
+  *c = {p.Gc * sc, sc, (int32_t)(p.N / p.Gc), 0};
+}
+
+}  // namespace
+
+extern "C" {
+
+ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
+                    int64_t page_bytes, ccl_plan_t* out) {
+  if (!out) return fail(CCL_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  ccl::Plan p;
+  std::string err;
+  ccl::Status s = ccl::make_plan(M, N, K, chiplets, grid_rows, page_bytes, &p, &err);
+  if (s != ccl::Status::OK) return from(s, err);
+  ccl_plan_s* h = new (std::nothrow) ccl_plan_s;
+  if (!h) return fail(CCL_ERR_INVALID_ARG, "out of host memory");
+  h->plan = p;
+  *out = h;
+  return ok();
+}
+
+ccl_status ccl_plan_destroy(ccl_plan_t plan) {
+  delete plan;
+  return ok();
+}
+
+ccl_status ccl_plan_grid(ccl_plan_t plan, int* grid_rows, int* grid_cols) {
+  if (!plan || !grid_rows || !grid_cols) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  *grid_rows = plan->plan.Gr;
+  *grid_cols = plan->plan.Gc;
+  return ok();
+}
+
+ccl_status ccl_plan_layout(ccl_plan_t plan, ccl_operand op, ccl_layout* out) {
+  if (!plan || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!valid_op(op)) return fail(CCL_ERR_INVALID_ARG, "operand must be CCL_A, CCL_B or CCL_C");
+  const ccl::Layout& l = plan->plan.lay[op];
+  out->rows = l.rows;
+  out->cols = l.cols;
+  out->grid_r = l.grid_r;
+  out->grid_c = l.grid_c;
+  out->block_rows = l.block_rows;
+  out->block_cols = l.block_cols;
+  out->strip_bytes = l.strip_bytes;
+  out->strip_stride_bytes = l.strip_stride_bytes;
+  out->total_bytes = l.total_bytes;
+  return ok();
+}
+
+ccl_status ccl_pack(ccl_plan_t plan, ccl_operand op, const void* src, int64_t ld, int src_trans,
+                    void* dst_ccl, void* stream) {
+  if (!plan || !src || !dst_ccl) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!valid_op(op)) return fail(CCL_ERR_INVALID_ARG, "operand must be CCL_A, CCL_B or CCL_C");
+  if (src_trans != 0 && src_trans != 1) return fail(CCL_ERR_INVALID_ARG, "src_trans must be 0 or 1");
+  if (src_trans && op == CCL_C) return fail(CCL_ERR_INVALID_ARG, "C has no stored-transpose form");
+  const ccl::Layout& l = plan->plan.lay[op];
+  if (ld < (src_trans ? l.rows : l.cols)) return fail(CCL_ERR_INVALID_ARG, "ld is smaller than the stored row");
+  if (l.block_rows * l.block_cols >= ((int64_t)1 << 31))
+    return fail(CCL_ERR_UNSUPPORTED, "a CCL strip of 2^31 elements or more is not supported");
+  if (ccl_status s = check_device()) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (src_trans) return hip_status(ccl::launch_pack_trans(plan->plan, op, src, ld, dst_ccl, st), "pack_trans launch");
+  return hip_status(ccl::launch_copy(plan->plan, op, src, ld, dst_ccl, false, st), "pack launch");
+}
+
+ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void* dst, int64_t ld,
+                      void* stream) {
+  if (!plan || !src_ccl || !dst) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!valid_op(op)) return fail(CCL_ERR_INVALID_ARG, "operand must be CCL_A, CCL_B or CCL_C");
+  const ccl::Layout& l = plan->plan.lay[op];
+  if (ld < l.cols) return fail(CCL_ERR_INVALID_ARG, "ld is smaller than the operand's columns");
+  if (l.block_rows * l.block_cols >= ((int64_t)1 << 31))
+    return fail(CCL_ERR_UNSUPPORTED, "a CCL strip of 2^31 elements or more is not supported");
+  if (ccl_status s = check_device()) return s;
+  return hip_status(ccl::launch_copy(plan->plan, op, dst, ld, const_cast<void*>(src_ccl), true,
+                                     static_cast<hipStream_t>(stream)),
+                    "unpack launch");
+}
+
+ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
+                    void* stream) {
+  if (!plan || !A_ccl || !B_ccl || !C_ccl) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!aligned16(A_ccl) || !aligned16(B_ccl) || !aligned16(C_ccl))
+    return fail(CCL_ERR_MISALIGNED_POINTER, "A, B and C must be 16-byte aligned");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  if (ccl_status s = check_device()) return s;
+  ccl::OperandAddr a, b, c;
+  ccl_addressing(p, &a, &b, &c);
+  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true,
+                                     static_cast<hipStream_t>(stream)),
+                    "gemm launch");
+}
+
+ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+                            ccl_traffic* out) {
+  if (!plan || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (placement != CCL_PLACE_RR && placement != CCL_PLACE_COARSE && placement != CCL_PLACE_CCL)
+    return fail(CCL_ERR_INVALID_ARG, "unknown placement");
+  if (stored_trans_mask < 0 || stored_trans_mask > 3)
+    return fail(CCL_ERR_INVALID_ARG, "stored_trans_mask must be in 0..3");
+  ccl::Traffic t = ccl::remote_bytes(plan->plan, static_cast<ccl::Placement>(placement), stored_trans_mask);
+  std::memset(out, 0, sizeof(*out));
+  for (int i = 0; i < 3; ++i) {
+    out->accessed[i] = t.accessed[i];
+    out->remote[i] = t.remote[i];
+    out->footprint[i] = t.footprint[i];
+  }
+  out->floor_bytes = t.floor_bytes;
+  for (int i = 0; i < t.chiplets; ++i) out->remote_per_chiplet[i] = t.remote_per_chiplet[i];
+  out->chiplets = t.chiplets;
+  return ok();
+}
+
+const char* ccl_status_string(ccl_status status) {
+  switch (status) {
+    case CCL_OK: return "CCL_OK";
+    case CCL_ERR_INVALID_ARG: return "CCL_ERR_INVALID_ARG";
+    case CCL_ERR_UNALIGNED_PARTITION: return "CCL_ERR_UNALIGNED_PARTITION";
+    case CCL_ERR_UNSUPPORTED: return "CCL_ERR_UNSUPPORTED";
+    case CCL_ERR_MISALIGNED_POINTER: return "CCL_ERR_MISALIGNED_POINTER";
+    case CCL_ERR_HIP: return "CCL_ERR_HIP";
+  }
+  return "CCL_ERR_UNKNOWN";
+}
+
+const char* ccl_last_error(void) { return g_last_error.c_str(); }
+
+ccl_status ccl_debug_tile_of_wg(ccl_plan_t plan, int64_t wg, int* xcd, int64_t* tile_m,
+                                int64_t* tile_n) {
+  if (!plan || !xcd || !tile_m || !tile_n) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!plan->plan.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, plan->plan.gemm.why_unsupported);
+  ccl::tile_of_wg(plan->plan, wg, xcd, tile_m, tile_n);
+  return ok();
+}
+
+ccl_status ccl_debug_gemm_config(ccl_plan_t plan, int* tile_rows, int* tile_cols,
+                                 int64_t* workgroups) {
+  if (!plan || !tile_rows || !tile_cols || !workgroups) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!plan->plan.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, plan->plan.gemm.why_unsupported);
+  *tile_rows = plan->plan.gemm.tile_m;
+  *tile_cols = plan->plan.gemm.tile_n;
+  *workgroups = plan->plan.gemm.workgroups;
+  return ok();
+}
+
+ccl_status ccl_debug_dispatch(ccl_plan_t plan, int32_t* out, void* stream) {
+  if (!plan || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (!plan->plan.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, plan->plan.gemm.why_unsupported);
+  if (ccl_status s = check_device()) return s;
+  return hip_status(ccl::launch_dispatch_probe(plan->plan, out, static_cast<hipStream_t>(stream)),
+                    "dispatch probe launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,94 @@
+// Host-side plan of a CCL GEMM: validation, per-operand CCL layouts, tile
+// ownership, the workgroup -> XCD -> tile map of the GEMM launch, and the
+// remote-byte model. Plain C++17, no HIP dependency.
+#pragma once
+
+#include <cstdint>
+#include <string>
+
+#include "tile_map.hpp"
+
+namespace ccl {
+
+constexpr int kModelTile = 128;   // output tile of the traffic model (Sec. IV-A)
+constexpr int kElemBytes = 2;     // bf16
+constexpr int kNumXcd = 8;        // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr int kMaxChiplets = 64;
+constexpr int kGemmBK = 64;       // K extent of one GEMM main-loop step
+
+enum Op { OP_A = 0, OP_B = 1, OP_C = 2 };
+enum Placement { PLACE_RR = 0, PLACE_COARSE = 1, PLACE_CCL = 2 };
+
+struct Layout {
+  int64_t rows = 0, cols = 0;
+  int64_t grid_r = 0, grid_c = 0;
+  int64_t block_rows = 0, block_cols = 0;
+  int64_t strip_bytes = 0, strip_stride_bytes = 0, total_bytes = 0;
+
+  // Byte offset of logical element (r, c) (Sec. III-B, block form of Eq. 3).
+  int64_t offset(int64_t r, int64_t c) const {
+    int64_t b = (r / block_rows) * grid_c + (c / block_cols);
+    return b * strip_stride_bytes + ((r % block_rows) * block_cols + (c % block_cols)) * kElemBytes;
+  }
+};
+
+// Kernel-level tiling chosen for a plan (kernel tiles nest inside partitions).
+struct GemmConfig {
+  int tile_m = 0, tile_n = 0;       // kernel output tile
+  int64_t tiles_m = 0, tiles_n = 0; // kernel tiles per partition
+  int xcd_per_chiplet = 0;          // 8 / G
+  int64_t tiles_per_xcd = 0;        // ceil(tiles per partition / xcd_per_chiplet)
+  int64_t workgroups = 0;           // 8 * tiles_per_xcd
+  int group_m = 0;                  // raster group height (tiles) inside a partition
+  bool supported = false;           // whether ccl_gemm can run this plan
+  std::string why_unsupported;
+};
+
+struct Traffic {
+  uint64_t accessed[3] = {0, 0, 0};
+  uint64_t remote[3] = {0, 0, 0};
+  uint64_t floor_bytes = 0;
+  uint64_t footprint[3] = {0, 0, 0};
+  uint64_t remote_per_chiplet[kMaxChiplets] = {};
+  int chiplets = 0;
+};
+
+struct Plan {
+  int64_t M = 0, N = 0, K = 0;
+  int G = 0, Gr = 0, Gc = 0;
+  int64_t page = 0;
+  Layout lay[3];
+  GemmConfig gemm;
+
+  int64_t part_rows() const { return M / Gr; }
+  int64_t part_cols() const { return N / Gc; }
+  // Chiplet owning the 128x128 model tile (ti, tj).
+  int owner(int64_t ti, int64_t tj) const {
+    return static_cast<int>((ti * kModelTile / part_rows()) * Gc + (tj * kModelTile / part_cols()));
+  }
+};
+
+enum class Status { OK = 0, INVALID_ARG = 1, UNALIGNED = 2, UNSUPPORTED = 3, MISALIGNED = 4, HIP = 5 };
+
+// Build a plan. grid_rows == 0 chooses the grid. On error returns the status
+// and fills `err` with a message.
+Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, int64_t page,
+                 Plan* out, std::string* err);
+
+// Whether a Gr x (G/Gr) grid gives tile-aligned partitions.
+bool grid_aligned(int64_t M, int64_t N, int64_t K, int G, int Gr);
+
+// Remote bytes of CCL (the floor): e*M*N*K*[(Gc-1)/(Gc*128) + (Gr-1)/(Gr*128)].
+uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc);
+
+// The remote-byte model under one placement. Stored-transpose flags apply
+// to A and B (bit 0, bit 1).
+Traffic remote_bytes(const Plan& p, Placement pl, int trans_mask);
+
+// Parameters of the workgroup -> tile map of the GEMM launch.
+TileMap tile_map(const Plan& p);
+
+// Workgroup -> (xcd, kernel tile) of the GEMM launch; tile = (-1, -1) if idle.
+void tile_of_wg(const Plan& p, int64_t wg, int* xcd, int64_t* tile_m, int64_t* tile_n);
+
+}  // namespace ccl

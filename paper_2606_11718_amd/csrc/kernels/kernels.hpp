@@ -1,0 +1,36 @@
+// Kernel launchers of the CCL library (device side lives in *.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../host/plan.hpp"
+
+namespace ccl {
+
+// Operand addressing of the GEMM kernel, in elements. Logical element
+// (m, k) of A with m in partition row pr and k in K-slice kc sits at
+//   A + pr * a_part + kc * a_slice + (m - pr*hr) * a_ld + (k - kc*a_kslice)
+// (B and C likewise). CCL: a_part = Gc*S, a_slice = S, a_ld = K/Gc.
+struct OperandAddr {
+  int64_t part;     // stride between partition blocks along the tile grid
+  int64_t slice;    // stride between K slices (A, B) / grid columns (C)
+  int32_t ld;       // leading dimension inside a block
+  int32_t kslice;   // K extent of one block (A, B); unused for C
+};
+
+// Pack (row-major -> CCL) or unpack (CCL -> row-major) with ld.
+hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, void* ccl_buf,
+                       bool unpack, hipStream_t stream);
+// Pack from a stored transpose (cols x rows, leading dimension ld).
+hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld, void* dst,
+                             hipStream_t stream);
+// C = A B with the given operand addressing; remap = XCD-aware tile map.
+hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
+                       const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
+                       bool remap, hipStream_t stream);
+// Dispatch probe with the GEMM grid (4 int32 per workgroup).
+hipError_t launch_dispatch_probe(const Plan& p, int32_t* out, hipStream_t stream);
+
+}  // namespace ccl

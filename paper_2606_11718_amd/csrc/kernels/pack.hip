@@ -1,0 +1,228 @@
+// Pack / unpack between row-major (or stored-transpose) bf16 operands and
+// the Chiplet-Contiguous Layout (Sec. III-B, Eq. 3 in block form):
+//   block b = (r / hr) * Gc + c / wc
+//   elem offset = b * S + (r % hr) * wc + c % wc     (S = padded strip, elements)
+//
+// The work is enumerated in CCL order: block b, then its q-th element (or
+// 16-byte chunk) in strip order, so every thread's CCL access is the next
+// contiguous piece of a strip and its row-major access is a contiguous run
+// of one row slice. Division by the run length uses a host-computed
+// multiplier. These kernels move bytes only; they are bound by HBM.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.hpp"
+
+namespace ccl {
+
+namespace {
+
+// q / d for q < 2^31, d < 2^31: multiply by ceil(2^s / d), s = 31 + ceil(log2 d).
+struct DivMagic {
+  uint64_t mul;
+  uint32_t shift;
+  uint32_t d;
+};
+
+DivMagic make_div(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  DivMagic m;
+  m.shift = 31 + l;
+  m.mul = (((uint64_t)1 << m.shift) + d - 1) / d;
+  m.d = d;
+  return m;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t q, const DivMagic& m) {
+  return (uint32_t)(((uint64_t)q * m.mul) >> m.shift);
+}
+
+struct PackArgs {
+  const uint16_t* rm;      // row-major side
+  uint16_t* rm_out;        // row-major side when written (unpack)
+  const uint16_t* ccl;     // CCL side (read by unpack)
+  uint16_t* ccl_out;       // CCL side (written by pack)
+  int64_t ld;              // row-major leading dimension, elements
+  int64_t strip;           // padded strip stride, elements
+  int64_t hr, wc;          // block rows / cols
+  int32_t grid_c;
+  uint32_t units_per_block;  // hr * wc / V
+  DivMagic units_per_row;    // wc / V
+};
+
+// V = elements per unit (8: one 16-byte vector, 1: one element).
+// UNPACK = false: row-major -> CCL; true: CCL -> row-major.
+template <int V, bool UNPACK>
+__global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
+  const int32_t b = blockIdx.y;                      // strip / chiplet
+  const int64_t pr = b / a.grid_c, pc = b % a.grid_c;
+  const uint16_t* src_rm = a.rm + pr * a.hr * a.ld + pc * a.wc;
+  uint16_t* dst_rm = a.rm_out + pr * a.hr * a.ld + pc * a.wc;
+  const int64_t strip_base = (int64_t)b * a.strip;
+  constexpr int UNROLL = 4;
+  const uint32_t stride = gridDim.x * 256u;
+  for (uint32_t base = blockIdx.x * 256u * UNROLL; base < a.units_per_block; base += stride * UNROLL) {
+    using T = typename std::conditional<V == 8, uint4, uint16_t>::type;
+    T v[UNROLL];
+    int64_t rm_off[UNROLL];
+    bool ok[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const uint32_t q = base + threadIdx.x + u * 256u;
+      ok[u] = q < a.units_per_block;
+      const uint32_t row = fdiv(q, a.units_per_row);
+      const uint32_t col = (q - row * a.units_per_row.d) * V;
+      rm_off[u] = (int64_t)row * a.ld + col;
+      if (ok[u]) {
+        if (UNPACK)
+          v[u] = *reinterpret_cast<const T*>(a.ccl + strip_base + (int64_t)q * V);
+        else
+          v[u] = *reinterpret_cast<const T*>(src_rm + rm_off[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const uint32_t q = base + threadIdx.x + u * 256u;
+      if (ok[u]) {
+        if (UNPACK)
+          *reinterpret_cast<T*>(dst_rm + rm_off[u]) = v[u];
+        else
+          *reinterpret_cast<T*>(a.ccl_out + strip_base + (int64_t)q * V) = v[u];
+      }
+    }
+  }
+}
+
+// Stored-transpose pack: src holds X^T (cols x rows, leading dimension ld),
+// X is rows x cols. A 64 x 64 tile is read along X's rows (contiguous in
+// src), transposed through LDS and written along X's columns (contiguous in
+// the CCL strip). Tiles never straddle blocks (hr, wc multiples of 64).
+struct TransArgs {
+  const uint16_t* src;
+  uint16_t* dst;
+  int64_t ld;
+  int64_t strip;
+  int64_t hr, wc;
+  int32_t grid_c;
+  int32_t tiles_c;         // cols / 64
+};
+
+__global__ void __launch_bounds__(256) pack_trans_kernel(TransArgs a) {
+  __shared__ uint16_t tile[64][64 + 8];
+  const int64_t r0 = (int64_t)blockIdx.y * 64;        // X rows = src columns
+  const int64_t c0 = (int64_t)blockIdx.x * 64;        // X cols = src rows
+  const int t = threadIdx.x;
+  // read: src rows c0..c0+63, 64 elements each = 8 chunks of 16 B
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int idx = t + i * 256;
+    const int sr = idx >> 3, ch = idx & 7;
+    uint4 v = *reinterpret_cast<const uint4*>(a.src + (c0 + sr) * a.ld + r0 + ch * 8);
+    const uint16_t* e = reinterpret_cast<const uint16_t*>(&v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tile[sr][ch * 8 + j] = e[j];
+  }
+  __syncthreads();
+  // write: X row r0+xr, columns c0 + 8*ch .. +8, contiguous in the strip
+  const int64_t pr = r0 / a.hr, pc = c0 / a.wc;
+  const int64_t b = pr * a.grid_c + pc;
+  uint16_t* strip = a.dst + b * a.strip;
+  const int64_t rl0 = r0 - pr * a.hr, cl0 = c0 - pc * a.wc;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int idx = t + i * 256;
+    const int xr = idx >> 3, ch = idx & 7;
+    uint4 v;
+    uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e[j] = tile[ch * 8 + j][xr];
+    *reinterpret_cast<uint4*>(strip + (rl0 + xr) * a.wc + cl0 + ch * 8) = v;
+  }
+}
+
+// Any shape: one element per thread, src holds X^T.
+__global__ void __launch_bounds__(256) pack_trans_scalar_kernel(TransArgs a, int64_t rows,
+                                                                int64_t cols) {
+  const int64_t n = rows * cols;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t r = i / cols, c = i % cols;          // write order: along X rows
+    const int64_t pr = r / a.hr, pc = c / a.wc;
+    const int64_t b = pr * a.grid_c + pc;
+    a.dst[b * a.strip + (r - pr * a.hr) * a.wc + (c - pc * a.wc)] = a.src[c * a.ld + r];
+  }
+}
+
+int grid_x_for(uint32_t units, int unroll) {
+  uint64_t wgs = ((uint64_t)units + 256ull * unroll - 1) / (256ull * unroll);
+  if (wgs > 4096) wgs = 4096;
+  return (int)(wgs ? wgs : 1);
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, void* ccl_buf,
+                       bool unpack, hipStream_t stream) {
+  const Layout& L = p.lay[op];
+  const bool vec = (L.block_cols % 8 == 0) && (ld % 8 == 0) && aligned16(rowmajor) &&
+                   aligned16(ccl_buf) && (L.strip_stride_bytes % 16 == 0);
+  const int V = vec ? 8 : 1;
+  PackArgs a;
+  a.rm = static_cast<const uint16_t*>(rowmajor);
+  a.rm_out = const_cast<uint16_t*>(static_cast<const uint16_t*>(rowmajor));
+  a.ccl = static_cast<const uint16_t*>(ccl_buf);
+  a.ccl_out = static_cast<uint16_t*>(ccl_buf);
+  a.ld = ld;
+  a.strip = L.strip_stride_bytes / 2;
+  a.hr = L.block_rows;
+  a.wc = L.block_cols;
+  a.grid_c = (int32_t)L.grid_c;
+  a.units_per_block = (uint32_t)(L.block_rows * L.block_cols / V);
+  a.units_per_row = make_div((uint32_t)(L.block_cols / V));
+  dim3 grid(grid_x_for(a.units_per_block, 4), (unsigned)(L.grid_r * L.grid_c));
+  if (vec) {
+    if (unpack)
+      hipLaunchKernelGGL((copy_kernel<8, true>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((copy_kernel<8, false>), grid, dim3(256), 0, stream, a);
+  } else {
+    if (unpack)
+      hipLaunchKernelGGL((copy_kernel<1, true>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((copy_kernel<1, false>), grid, dim3(256), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld, void* dst,
+                             hipStream_t stream) {
+  const Layout& L = p.lay[op];
+  TransArgs a;
+  a.src = static_cast<const uint16_t*>(src);
+  a.dst = static_cast<uint16_t*>(dst);
+  a.ld = ld;
+  a.strip = L.strip_stride_bytes / 2;
+  a.hr = L.block_rows;
+  a.wc = L.block_cols;
+  a.grid_c = (int32_t)L.grid_c;
+  const bool tiled = L.block_rows % 64 == 0 && L.block_cols % 64 == 0 && ld % 8 == 0 &&
+                     aligned16(src) && aligned16(dst) && L.strip_stride_bytes % 16 == 0 &&
+                     L.rows / 64 <= 65535;
+  if (tiled) {
+    a.tiles_c = (int32_t)(L.cols / 64);
+    dim3 grid((unsigned)(L.cols / 64), (unsigned)(L.rows / 64));
+    hipLaunchKernelGGL(pack_trans_kernel, grid, dim3(256), 0, stream, a);
+  } else {
+    int64_t n = L.rows * L.cols;
+    int64_t wgs = (n + 255) / 256;
+    if (wgs > 8192) wgs = 8192;
+    hipLaunchKernelGGL(pack_trans_scalar_kernel, dim3((unsigned)wgs), dim3(256), 0, stream, a,
+                       L.rows, L.cols);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ccl

@@ -1,0 +1,178 @@
+"""GPU parity of ccl_gemm with the fp64 oracle (Sec. II-B C = A B).
+
+Tolerance: relative Frobenius error <= 5e-3 and max abs error <= 1e-2 *
+max|C_ref|. C is read back through the oracle's own unpack of the GPU's CCL
+buffer. Workloads that the host can multiply in fp64 are compared in full;
+the Llama-sized GEMMs on sampled output positions (each computed as an
+fp64 dot product by the oracle). Integer-valued cases are bit-exact.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import gemm as OG
+from oracle import layout as OL
+from oracle import plan as OP
+from paper_2606_11718_amd import ccl
+from tests.helpers import CANARY, dev_full, from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None, unpack=True):
+    """Pack A and B on the GPU and run the GEMM. Returns (C, plan) where C is
+    the row-major bf16 bits (oracle unpack), or (ccl buffer, Gr, Gc) when
+    unpack is False."""
+    if tile:
+        os.environ["CCL_GEMM_TILE"] = tile
+    try:
+        plan = ccl.ccl_plan(M, N, K, G, Gr, P)
+    finally:
+        os.environ.pop("CCL_GEMM_TILE", None)
+    gr, gc = ccl.ccl_plan_grid(plan)
+    tm_, tn_, wgs = ccl.ccl_debug_gemm_config(plan)
+    print(f"gemm {M}x{N}x{K} grid {gr}x{gc} P={P} tile {tm_}x{tn_} wgs={wgs} "
+          f"trans=({a_trans},{b_trans})", flush=True)
+    la, lb, lc = (ccl.ccl_plan_layout(plan, op) for op in (ccl.CCL_A, ccl.CCL_B, ccl.CCL_C))
+    Ad, Bd = to_dev(A_stored), to_dev(B_stored)
+    Ac, Bc, Cc = dev_full(la.total_bytes // 2), dev_full(lb.total_bytes // 2), dev_full(lc.total_bytes // 2)
+    ccl.ccl_pack(plan, ccl.CCL_A, Ad, A_stored.shape[1], a_trans, Ac)
+    ccl.ccl_pack(plan, ccl.CCL_B, Bd, B_stored.shape[1], b_trans, Bc)
+    del Ad, Bd
+    ccl.ccl_gemm(plan, Ac, Bc, Cc)
+    cbuf = from_dev(Cc)
+    if lc.total_bytes != lc.strip_bytes * gr * gc:       # padding untouched
+        assert np.all(cbuf[OL.padding_mask(M, N, gr, gc, P)] == CANARY)
+    return (OL.unpack(cbuf, M, N, gr, gc, P) if unpack else (cbuf, gr, gc)), plan
+
+
+def _logical(stored, trans):
+    return np.ascontiguousarray(stored.T) if trans else stored
+
+
+def _check_full(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None):
+    Cbits, _ = run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile)
+    C_ref = OG.gemm_fp64(_logical(A_stored, a_trans), _logical(B_stored, b_trans))
+    err = OG.errors(OG.decode_bf16(Cbits), C_ref)
+    print("errors", err, flush=True)
+    assert err["rel_fro"] <= 5e-3
+    assert err["max_abs"] <= 1e-2 * err["max_ref"]
+    return err
+
+
+@pytest.mark.parametrize("gemm", ["tiny", "qwen_gate_up", "qwen_dW_down", "qwen_dH"])
+def test_gemm_workloads_full_compare(gemm):
+    wl, g = W.gemm_by_name(gemm)
+    A = W.draw(wl.tensors[g.a_src])
+    B = W.draw(wl.tensors[g.b_src])
+    _check_full(A, g.a_trans, B, g.b_trans, g.M, g.N, g.K, g.chiplets, g.grids[0], g.pages[0])
+
+
+def test_qwen_backward_grids_are_the_automatic_choice():
+    for name, expect in (("qwen_dW_down", 1), ("qwen_dH", 8)):
+        _, g = W.gemm_by_name(name)
+        p = ccl.ccl_plan(g.M, g.N, g.K, g.chiplets, 0, 4096)
+        assert ccl.ccl_plan_grid(p)[0] == expect == OP.auto_grid_rows(g.M, g.N, g.K, g.chiplets)
+
+
+@pytest.mark.parametrize("tile", ["256x256", "256x128", "128x256", "128x128"])
+def test_gemm_every_kernel_tile(tile):
+    M, N, K = 2048, 2048, 1024
+    A = W.draw_array(901, M, K, "normal", 1.0)
+    B = W.draw_array(902, K, N, "normal", 0.02)
+    _check_full(A, 0, B, 0, M, N, K, 8, 2, 4096, tile)
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr,P,ta,tb", [
+    (256, 512, 256, 4, 2, 65536, 0, 0),          # padded strips
+    (256, 512, 256, 4, 2, 2 * 1024 * 1024, 0, 1),
+    (512, 512, 512, 1, 1, 4096, 1, 0),           # one chiplet: all XCDs share the partition
+    (1024, 2048, 512, 2, 1, 4096, 0, 0),         # 2 chiplets of 4 XCDs
+    (1024, 1024, 512, 8, 8, 4096, 1, 1),         # 8x1: K slices of 64 rows for B
+    (1024, 1024, 512, 8, 1, 4096, 0, 0),         # 1x8: K slices of 64 columns for A
+    (2048, 384, 256, 4, 4, 4096, 0, 1),          # 4x1 with one K step per B slice
+    (128, 128, 64, 1, 1, 4096, 0, 0),            # single tile, single K step
+])
+def test_gemm_edge_shapes(M, N, K, G, Gr, P, ta, tb):
+    A = W.draw_array(1000 + M + K, *((K, M) if ta else (M, K)), "normal", 1.0)
+    B = W.draw_array(2000 + N + K, *((N, K) if tb else (K, N)), "normal", 0.5)
+    _check_full(A, ta, B, tb, M, N, K, G, Gr, P)
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(256, 512, 256, 4, 2), (1024, 2048, 256, 8, 2), (1024, 1024, 512, 8, 8)])
+def test_gemm_integer_inputs_bit_exact(M, N, K, G, Gr):
+    """Values in {-1, 0, 1} with K <= 512: every partial sum is an integer
+    of magnitude <= 512, exact in fp32; |C| <= 256 in these draws' bounds
+    is checked and then C must equal the integer product exactly."""
+    A = W.draw_array(31, M, K, "ternary")
+    B = W.draw_array(32, K, N, "ternary")
+    ref = OG.decode_bf16(A).astype(np.int64) @ OG.decode_bf16(B).astype(np.int64)
+    assert np.abs(ref).max() <= 256          # representable exactly in bf16
+    Cbits, _ = run_gemm(A, 0, B, 0, M, N, K, G, Gr, 4096)
+    assert np.array_equal(OG.decode_bf16(Cbits), ref.astype(np.float64))
+
+
+def test_gemm_identity_returns_a_bit_exact():
+    M, K = 512, 512
+    A = W.draw_array(41, M, K, "normal", 3.0)
+    I = W.round_to_bf16_bits(np.eye(K, dtype=np.float32))
+    Cbits, _ = run_gemm(A, 0, I, 0, M, K, K, 4, 2, 4096)
+    assert np.array_equal(Cbits, A)
+
+
+def _sampled_check(gemm, grid, n_samples=4096, seed=0):
+    wl, g = W.gemm_by_name(gemm)
+    A = W.draw(wl.tensors[g.a_src])
+    B = W.draw(wl.tensors[g.b_src])
+    (cbuf, gr, gc), _ = run_gemm(A, g.a_trans, B, g.b_trans, g.M, g.N, g.K, g.chiplets, grid, 4096,
+                                  unpack=False)
+    rng = np.random.default_rng(seed)
+    rows = rng.integers(0, g.M, n_samples)
+    cols = rng.integers(0, g.N, n_samples)
+    # always include the corners of every partition
+    pr_rows = [r for p in range(gr) for r in (p * g.M // gr, (p + 1) * g.M // gr - 1)]
+    pc_cols = [c for p in range(gc) for c in (p * g.N // gc, (p + 1) * g.N // gc - 1)]
+    rows = np.concatenate([rows, np.repeat(pr_rows, len(pc_cols))])
+    cols = np.concatenate([cols, np.tile(pc_cols, len(pr_rows))])
+    Al = A[:, rows].T if g.a_trans else A[rows]
+    Bl = B[cols, :].T if g.b_trans else B[:, cols]
+    ref = OG.gemm_entries(Al, Bl, np.arange(len(rows)), np.arange(len(cols)))
+    off = OL.ccl_offset(rows, cols, g.M, g.N, gr, gc, 4096) // 2
+    got = OG.decode_bf16(cbuf[off])
+    err = OG.errors(got, ref)
+    print(gemm, grid, "sampled errors", err, flush=True)
+    assert err["rel_fro"] <= 5e-3
+    assert err["max_abs"] <= 1e-2 * err["max_ref"]
+
+
+@pytest.mark.parametrize("gemm", ["llama_up", "llama_down"])
+def test_gemm_llama_forward_sampled(gemm):
+    _sampled_check(gemm, 2)
+
+
+@pytest.mark.parametrize("gemm", ["llama_dW_up", "llama_dX"])
+@pytest.mark.parametrize("grid", [1, 2, 4, 8])
+def test_gemm_llama_backward_grid_sweep_sampled(gemm, grid):
+    _sampled_check(gemm, grid, n_samples=2048, seed=grid)
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(8192, 28672, 8192, 8, 2), (768, 2048, 4096, 8, 1),
+                                        (4096, 768, 2048, 8, 8), (256, 512, 256, 4, 2),
+                                        (1024, 1024, 1024, 1, 1), (1024, 2048, 512, 2, 1)])
+def test_dispatch_probe_tiles_run_on_owner_xcd(M, N, K, G, Gr):
+    """Hardware check of the remap: each workgroup's XCC id is wg mod 8 and
+    lies in the owning chiplet's XCDs; every tile is computed exactly once."""
+    torch = __import__("torch")
+    plan = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+    tm_, tn_, wgs = ccl.ccl_debug_gemm_config(plan)
+    out = torch.full((4 * wgs,), -7, dtype=torch.int32, device="cuda")
+    ccl.ccl_debug_dispatch(plan, out)
+    rec = out.cpu().numpy().reshape(wgs, 4)
+    assert np.array_equal(rec[:, 0], np.arange(wgs) % 8)
+    live = rec[rec[:, 1] >= 0]
+    assert len({(a, b) for a, b in live[:, 1:3]}) == len(live) == (M // tm_) * (N // tn_)
+    for xcd, ti, tj, owner in live:
+        assert owner == OP.owner(ti * tm_ // 128, tj * tn_ // 128, M, N, Gr, G // Gr)
+        assert xcd in OP.xcds_of_chiplet(owner, G)

@@ -1,0 +1,186 @@
+"""CPU tests of the HIP library's host side, through the C ABI.
+
+No GPU: the library loads, exports every symbol the header declares, and its
+host-only calls (plan, layouts, remote-byte model, workgroup -> tile map)
+match the oracle bit for bit.
+"""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from oracle import plan as OP
+from oracle import traffic as OT
+from paper_2606_11718_amd import ccl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ccl.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "traffic_golden.json")
+PLACE = {"rr": ccl.CCL_PLACE_RR, "coarse": ccl.CCL_PLACE_COARSE, "ccl": ccl.CCL_PLACE_CCL}
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return re.findall(r"^(?:ccl_status|const char\*)\s+(ccl_\w+)\(", text, re.M)
+
+
+def test_library_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 10
+    ccl.library()          # loads the HIP runtime torch uses, then libccl.so
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_11718_amd", "libccl.so"))
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(ccl.EXPORTED)
+
+
+def test_status_strings():
+    assert ccl.ccl_status_string(0) == "CCL_OK"
+    assert ccl.ccl_status_string(2) == "CCL_ERR_UNALIGNED_PARTITION"
+    assert ccl.ccl_status_string(99) == "CCL_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 512, 256, 4, 2, 4096), 1),          # empty M
+    ((256, 512, 0, 4, 2, 4096), 1),          # empty K
+    ((256, 512, 256, 0, 0, 4096), 1),        # no chiplets
+    ((256, 512, 256, 65, 0, 4096), 1),       # too many chiplets
+    ((256, 512, 256, 4, 3, 4096), 1),        # grid does not divide
+    ((256, 512, 256, 4, -1, 4096), 1),
+    ((256, 512, 256, 4, 2, 3000), 1),        # page not a power of two
+    ((256, 512, 256, 4, 2, 64), 1),          # page too small
+    ((256, 512, 256, 4, 4, 4096), 2),        # 256 rows / 4 is not a tile
+    ((256, 500, 256, 4, 2, 4096), 2),        # ragged N
+    ((256, 512, 255, 4, 2, 4096), 2),        # K not divisible by the grid
+    ((100, 100, 100, 8, 0, 4096), 2),        # automatic: no aligned grid
+    ((1 << 31, 128, 128, 1, 1, 4096), 1),    # overflow guard
+])
+def test_plan_rejections(args, status):
+    with pytest.raises(ccl.CCLError) as ei:
+        ccl.ccl_plan(*args)
+    assert ei.value.status == status
+    assert ccl.ccl_last_error() != ""
+
+
+def test_null_arguments_are_rejected_without_gpu():
+    p = ccl.ccl_plan(256, 512, 256, 4, 2, 4096)
+    lib = ccl.library()
+    assert lib.ccl_plan_layout(p, 0, None) == 1
+    assert lib.ccl_plan_layout(p, 7, ctypes.byref(ccl._Layout())) == 1
+    assert lib.ccl_remote_bytes(p, 5, 0, ctypes.byref(ccl._Traffic())) == 1
+    assert lib.ccl_remote_bytes(p, 0, 4, ctypes.byref(ccl._Traffic())) == 1
+    assert lib.ccl_gemm(p, None, None, None, None) == 1
+    assert lib.ccl_gemm(p, 16, 32, 8, None) == 4            # misaligned pointer
+    assert lib.ccl_pack(p, 0, None, 256, 0, None, None) == 1
+    assert lib.ccl_pack(p, 2, 16, 512, 1, 16, None) == 1     # C has no transpose
+    assert lib.ccl_pack(p, 0, 16, 100, 0, 16, None) == 1     # ld < cols
+    assert lib.ccl_unpack(p, 1, 16, 16, 10, None) == 1
+    assert lib.ccl_plan_destroy(None) == 0
+    q = ccl.ccl_plan(256, 512, 192, 4, 2, 4096)             # K / Gc = 96: no GEMM kernel
+    with pytest.raises(ccl.CCLError) as ei:
+        ccl.ccl_gemm(q, 16, 16, 16)
+    assert ei.value.status == 3
+
+
+LAYOUT_CASES = [(256, 512, 256, 4, 2, 4096), (4096, 1536, 2048, 8, 2, 4096),
+                (768, 2048, 4096, 8, 1, 65536), (384, 768, 201, 3, 1, 2048),
+                (256, 512, 256, 4, 2, 2 * 1024 * 1024)]
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr,P", LAYOUT_CASES)
+def test_layouts_match_oracle(M, N, K, G, Gr, P):
+    p = ccl.ccl_plan(M, N, K, G, Gr, P)
+    Gc = G // Gr
+    for op, name in ((ccl.CCL_A, "A"), (ccl.CCL_B, "B"), (ccl.CCL_C, "C")):
+        R, Cc = OL.operand_shape(name, M, N, K)
+        lay = ccl.ccl_plan_layout(p, op)
+        hr, wc = OL.block_shape(R, Cc, Gr, Gc)
+        assert (lay.rows, lay.cols, lay.grid_r, lay.grid_c) == (R, Cc, Gr, Gc)
+        assert (lay.block_rows, lay.block_cols) == (hr, wc)
+        assert lay.strip_stride_bytes == OL.strip_stride_bytes(R, Cc, Gr, Gc, P)
+        assert lay.total_bytes == OL.total_bytes(R, Cc, Gr, Gc, P)
+
+
+@pytest.mark.parametrize("M,N,K,G", [(768, 2048, 4096, 8), (4096, 768, 2048, 8), (1024, 4096, 1024, 8),
+                                     (4096, 1024, 1024, 8), (256, 512, 256, 4), (8192, 28672, 8192, 8),
+                                     (512, 512, 512, 1), (1024, 1024, 1024, 2)])
+def test_auto_grid_matches_oracle(M, N, K, G):
+    p = ccl.ccl_plan(M, N, K, G, 0, 4096)
+    assert ccl.ccl_plan_grid(p)[0] == OP.auto_grid_rows(M, N, K, G)
+
+
+def _golden_records():
+    if not os.path.exists(GOLDEN):
+        pytest.skip("traffic_golden.json not generated")
+    return json.load(open(GOLDEN))["records"]
+
+
+def test_remote_bytes_match_oracle_golden_all_workloads():
+    """Every workload GEMM x grid x page x placement, bit-exact."""
+    recs = _golden_records()
+    assert len(recs) >= 90
+    for r in recs:
+        p = ccl.ccl_plan(r["M"], r["N"], r["K"], r["chiplets"], r["grid_rows_requested"], r["page"])
+        assert ccl.ccl_plan_grid(p)[0] == r["grid_rows"]
+        got = ccl.ccl_remote_bytes(p, PLACE[r["placement"]], r["trans_a"] | (r["trans_b"] << 1))
+        for k in ("accessed", "remote", "remote_per_chiplet", "floor", "footprint"):
+            assert got[k] == r[k], (r["gemm"], r["grid_rows"], r["page"], r["placement"], k)
+
+
+RANDOM_SHAPES = [
+    (256, 512, 256, 2, 2, 4096, 0, 0), (256, 256, 384, 1, 2, 256, 1, 0), (512, 256, 192, 4, 1, 512, 1, 1),
+    (384, 768, 201, 1, 3, 2048, 1, 0), (1024, 256, 320, 8, 1, 128, 0, 1), (256, 1024, 96, 1, 8, 65536, 0, 0),
+    (640, 384, 330, 5, 1, 1024, 1, 1), (256, 384, 300, 2, 3, 128, 0, 1), (128, 128, 7, 1, 1, 128, 1, 1),
+]
+
+
+@pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", RANDOM_SHAPES)
+@pytest.mark.parametrize("placement", OT.PLACEMENTS)
+def test_remote_bytes_match_oracle_small(M, N, K, Gr, Gc, P, ta, tb, placement):
+    p = ccl.ccl_plan(M, N, K, Gr * Gc, Gr, P)
+    got = ccl.ccl_remote_bytes(p, PLACE[placement], ta | (tb << 1))
+    ref = OT.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb)
+    for k in ("accessed", "remote", "remote_per_chiplet", "floor", "footprint"):
+        assert got[k] == ref[k], k
+
+
+TILE_CASES = [(256, 512, 256, 4, 2), (4096, 1536, 2048, 8, 2), (768, 2048, 4096, 8, 1),
+              (4096, 768, 2048, 8, 8), (8192, 28672, 8192, 8, 2), (8192, 8192, 28672, 8, 4),
+              (1024, 1024, 1024, 1, 1), (1024, 2048, 512, 2, 1), (2048, 384, 256, 4, 4)]
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", TILE_CASES)
+def test_workgroup_tile_map_covers_each_tile_once_on_owner_xcd(M, N, K, G, Gr):
+    """Round-robin dispatch puts workgroup w on XCD w mod 8; the map must send
+    every kernel tile exactly once to an XCD of the chiplet owning it."""
+    p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+    Gc = G // Gr
+    tm_, tn_, wgs = ccl.ccl_debug_gemm_config(p)
+    assert wgs % 8 == 0
+    seen = {}
+    for wg in range(wgs):
+        xcd, ti, tj = ccl.ccl_debug_tile_of_wg(p, wg)
+        assert xcd == wg % 8
+        if ti < 0:
+            continue
+        assert (ti, tj) not in seen
+        seen[(ti, tj)] = xcd
+        owner = OP.owner(ti * tm_ // 128, tj * tn_ // 128, M, N, Gr, Gc)
+        # every 128x128 model tile inside the kernel tile has the same owner
+        assert owner == OP.owner((ti * tm_ + tm_ - 1) // 128, (tj * tn_ + tn_ - 1) // 128, M, N, Gr, Gc)
+        assert xcd in OP.xcds_of_chiplet(owner, G)
+    assert len(seen) == (M // tm_) * (N // tn_)
+    # workgroups beyond the launch have no tile
+    assert ccl.ccl_debug_tile_of_wg(p, wgs)[1] == -1
+
+
+def test_gemm_config_tiles_nest_in_partitions():
+    for (M, N, K, G, Gr) in TILE_CASES:
+        p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+        tm_, tn_, _ = ccl.ccl_debug_gemm_config(p)
+        assert (M // Gr) % tm_ == 0 and (N // (G // Gr)) % tn_ == 0
+        assert tm_ in (128, 256) and tn_ in (128, 256)
