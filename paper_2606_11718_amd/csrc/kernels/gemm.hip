@@ -78,8 +78,23 @@ struct Tile {
   static constexpr int NB = BN / 32;                   // B load instructions per wave per stage
 };
 
+// MFMA operand fragments of one kk sub-step: A rows and B columns.
+template <int TM, int TN>
+struct FragSet {
+  bf16x8 a[TM];
+  bf16x8 b[TN];
+};
+
+// Instruction classes for __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedVmemRead = 0x020;
+constexpr int kSchedDsRead = 0x100;
+
 template <int BM, int BN>
 __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
+  // The host pass only needs the launch stub; the body uses device-only
+  // buffer-resource builtins.
+#if defined(__HIP_DEVICE_COMPILE__)
   using T = Tile<BM, BN>;
   __shared__ __attribute__((aligned(1024))) char smA0[T::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char smA1[T::A_BYTES];
@@ -110,21 +125,24 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
-  // ---- global -> LDS load offsets (elements), fixed for the whole loop ----
-  int32_t a_off[T::NA];
+  // ---- global -> LDS: per-lane byte offsets from the K step's tile corner ----
+  uint32_t a_voff[T::NA];
 #pragma unroll
   for (int i = 0; i < T::NA; ++i) {
     const int row = 8 * (wave * T::NA + i) + (lane >> 3);
     const int chunk = (lane & 7) ^ swz_a(row);
-    a_off[i] = row * p.a.ld + chunk * 8;
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
   }
-  int32_t b_off[T::NB];
+  uint32_t b_voff[T::NB];
 #pragma unroll
   for (int i = 0; i < T::NB; ++i) {
     const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
     const int chunk = (lane % T::CPR_B) ^ swz_b(row);
-    b_off[i] = row * p.b.ld + chunk * 8;
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 8) * 2u;
   }
+  // Bytes a K step may touch from its corner: loads outside return zero.
+  const int32_t a_extent = (BM - 1) * p.a.ld * 2 + kBK * 2;
+  const int32_t b_extent = (kBK - 1) * p.b.ld * 2 + BN * 2;
 
   // ---- LDS fragment read offsets (bytes) ----
   int32_t a_rd[4];
@@ -148,27 +166,54 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
     }
   }
 
-  // ---- operand base pointers ----
+  // ---- operand corners; K-slice block advances every kslice columns/rows ----
   const uint16_t* a_base = p.A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
   const uint16_t* b_base = p.B + pc * p.b.part + tj * BN;
-  int64_t a_slice_off = 0, b_slice_off = 0;    // current K-slice block
-  int32_t a_kl = 0, b_kl = 0;                  // K offset inside it
+  int64_t a_slice_off = 0, b_slice_off = 0;
+  int32_t a_kl = 0, b_kl = 0;
 
-  auto load_stage = [&](char* smA, char* smB) {
-    const uint16_t* ap = a_base + a_slice_off + a_kl;
-    const uint16_t* bp = b_base + b_slice_off + (int64_t)b_kl * p.b.ld;
+  // Issue the direct-to-LDS loads of the next K step. With live == false
+  // the descriptors cover zero bytes: every load is out of range, touches
+  // no memory and writes zeros to the (unused) stage.
+  auto load_stage = [&](char* smA, char* smB, bool live) {
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a_base + a_slice_off + a_kl), (short)0, live ? a_extent : 0, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(b_base + b_slice_off + (int64_t)b_kl * p.b.ld), (short)0, live ? b_extent : 0,
+        0x00020000);
 #pragma unroll
     for (int i = 0; i < T::NA; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(ap + a_off[i]),
-                                       (lds_void*)(smA + (wave * T::NA + i) * 1024), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(smA + (wave * T::NA + i) * 1024), 16,
+                                               a_voff[i], 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < T::NB; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(bp + b_off[i]),
-                                       (lds_void*)(smB + (wave * T::NB + i) * 1024), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(smB + (wave * T::NB + i) * 1024), 16,
+                                               b_voff[i], 0, 0, 0);
+    // advance to the next K step (branch-free; past the last step the
+    // corners are never used with a non-empty descriptor)
     a_kl += kBK;
-    if (a_kl == p.a.kslice) { a_kl = 0; a_slice_off += p.a.slice; }
+    const bool a_wrap = a_kl == p.a.kslice;
+    a_kl = a_wrap ? 0 : a_kl;
+    a_slice_off += a_wrap ? p.a.slice : 0;
     b_kl += kBK;
-    if (b_kl == p.b.kslice) { b_kl = 0; b_slice_off += p.b.slice; }
+    const bool b_wrap = b_kl == p.b.kslice;
+    b_kl = b_wrap ? 0 : b_kl;
+    b_slice_off += b_wrap ? p.b.slice : 0;
+  };
+
+  using Frags = FragSet<T::TM, T::TN>;
+  auto read_frags = [&](const char* smA, const char* smB, int kk, Frags& f) {
+#pragma unroll
+    for (int mt = 0; mt < T::TM; ++mt)
+      f.a[mt] = *(const lds_bf16x8*)(smA + a_rd[kk] + mt * 32 * 128);
+#pragma unroll
+    for (int nt = 0; nt < T::TN; ++nt) {
+      i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(smB + b_rd[nt][0] + kk * 16 * BN * 2));
+      i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(smB + b_rd[nt][1] + kk * 16 * BN * 2));
+      f.b[nt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
   };
 
   f32x16 acc[T::TM][T::TN];
@@ -179,43 +224,63 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto compute_stage = [&](const char* smA, const char* smB) {
+  auto mfmas = [&](const Frags& f) {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 af[T::TM], bfr[T::TN];
+    for (int mt = 0; mt < T::TM; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < T::TM; ++mt)
-        af[mt] = *(const lds_bf16x8*)(smA + a_rd[kk] + mt * 32 * 128);
+      for (int nt = 0; nt < T::TN; ++nt)
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[nt], f.a[mt], acc[mt][nt], 0, 0, 0);
+  };
+
+  constexpr int kMfmaPerKK = T::TM * T::TN;
+  constexpr int kReadsPerKK = T::TM + 2 * T::TN;
+  // Behind each MFMA issue at most one buffer load and one LDS read, so the
+  // matrix pipe stays fed while the memory instructions drain.
+  auto interleave = [&](int n_vmem) {
 #pragma unroll
-      for (int nt = 0; nt < T::TN; ++nt) {
-        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(smB + b_rd[nt][0] + kk * 16 * BN * 2));
-        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4*)(smB + b_rd[nt][1] + kk * 16 * BN * 2));
-        bfr[nt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      }
-#pragma unroll
-      for (int mt = 0; mt < T::TM; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < T::TN; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nt], af[mt], acc[mt][nt], 0, 0, 0);
+    for (int i = 0; i < kMfmaPerKK; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      if (i < n_vmem) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+      if (i < kReadsPerKK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
     }
+#pragma unroll
+    for (int i = kMfmaPerKK; i < n_vmem; ++i) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+#pragma unroll
+    for (int i = kMfmaPerKK; i < kReadsPerKK; ++i) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  Frags f0, f1;
+  // One K step on LDS stage (smA, smB), whose kk = 0 fragments are in f0.
+  // The next step's loads go to (nA, nB) (dummy when !live) and its kk = 0
+  // fragments are read into f0 at the end.
+  auto step = [&](const char* smA, const char* smB, char* nA, char* nB, bool live) {
+    load_stage(nA, nB, live);
+    read_frags(smA, smB, 1, f1);
+    mfmas(f0);
+    interleave(T::NA + T::NB);
+    read_frags(smA, smB, 2, f0);
+    mfmas(f1);
+    interleave(0);
+    read_frags(smA, smB, 3, f1);
+    mfmas(f0);
+    interleave(0);
+    // all of this stage is in registers; the next stage's loads must land
+    wait_vm_all();
+    __syncthreads();
+    read_frags(nA, nB, 0, f0);
+    mfmas(f1);
+    interleave(0);
   };
 
   const int32_t ksteps = p.ksteps;
-  load_stage(smA0, smB0);
+  load_stage(smA0, smB0, true);
   wait_vm_all();
   __syncthreads();
+  read_frags(smA0, smB0, 0, f0);
   for (int32_t s = 0; s < ksteps; s += 2) {
-    if (s + 1 < ksteps) load_stage(smA1, smB1);
-    compute_stage(smA0, smB0);
-    wait_vm_all();
-    __syncthreads();
-    if (s + 1 >= ksteps) break;
-    if (s + 2 < ksteps) load_stage(smA0, smB0);
-    compute_stage(smA1, smB1);
-    wait_vm_all();
-    __syncthreads();
+    step(smA0, smB0, smA1, smB1, s + 1 < ksteps);
+    if (s + 1 < ksteps) step(smA1, smB1, smA0, smB0, s + 2 < ksteps);
   }
 
   // ---- epilogue: lane holds C[m][n .. n+3] for each (mt, nt, q) ----
@@ -235,6 +300,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
       }
     }
   }
+#endif
 }
 
 // Records, per workgroup of the GEMM grid, the XCD it ran on and its tile.
