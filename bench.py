@@ -50,36 +50,41 @@ def measured_traffic(launch_flops_unused=None):
 
 
 def cpu_baseline(target_s: float):
-    """The oracle's fp64 GEMM on a row sample of the up-projection GEMM.
-
-    The bf16 operands are widened to float64 once, outside the timed call;
-    the timed call is the oracle's GEMM on those float64 values."""
+    """The oracle's fp64 GEMMs of the step (up and down projections) on a
+    row sample sized for about target_s seconds (the whole GEMMs if the host
+    is fast enough). The bf16 operands are widened to float64 once, outside
+    the timed calls; the timed calls are the oracle's GEMM."""
     import threadpoolctl
     import workloads as W
     from oracle import gemm as OG
 
-    wl, g = W.gemm_by_name("llama_up")
-    B = OG.decode_bf16(W.draw(wl.tensors[g.b_src]))
-    A_all = W.draw(wl.tensors[g.a_src])
+    wl, g_up = W.gemm_by_name("llama_up")
+    _, g_dn = W.gemm_by_name("llama_down")
+    ops = []
+    for g in (g_up, g_dn):
+        ops.append((W.draw(wl.tensors[g.a_src]), OG.decode_bf16(W.draw(wl.tensors[g.b_src]))))
     info = threadpoolctl.threadpool_info()
     threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
 
     def run(rows):
-        A = OG.decode_bf16(A_all[:rows])
-        t0 = time.perf_counter()
-        OG.gemm_fp64(A, B)
-        return time.perf_counter() - t0
+        t = 0.0
+        for A_bits, B in ops:
+            A = OG.decode_bf16(A_bits[:rows])
+            t0 = time.perf_counter()
+            OG.gemm_fp64(A, B)
+            t += time.perf_counter() - t0
+        return t
 
     run(32)                                   # warm the BLAS threads
     t_cal = run(128)
-    rows = int(min(g.M, 128 * target_s / max(t_cal, 1e-3)))
+    rows = int(min(g_up.M, 128 * target_s / max(t_cal, 1e-3)))
     rows = max(128, (rows // 64) * 64)
     t = run(rows)
-    flops = 2.0 * rows * g.N * g.K
+    flops = 2.0 * rows * (g_up.N * g_up.K + g_dn.N * g_dn.K)
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"fp64 oracle GEMM (numpy BLAS) of the first {rows} of 8192 rows of X "
-                      f"times W_up (8192x28672): {flops / 1e12:.3f} TFLOP in {t:.2f} s"}
+            "sample": f"fp64 oracle GEMMs (numpy BLAS) of the step, first {rows} of 8192 token rows "
+                      f"of X W_up and H W_down: {flops / 1e12:.3f} TFLOP in {t:.2f} s"}
 
 
 def main():
