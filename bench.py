@@ -49,6 +49,58 @@ def measured_traffic(launch_flops_unused=None):
     return t.get("hbm_bytes_per_launch")
 
 
+_SMI = {}
+
+
+def smi_sample():
+    """One reading of socket power (W) and the XCD clocks (MHz), in-process
+    through the amdsmi library (no subprocess)."""
+    try:
+        import amdsmi
+        if "h" not in _SMI:
+            amdsmi.amdsmi_init(amdsmi.AmdSmiInitFlags.INIT_AMD_GPUS)
+            _SMI["h"] = amdsmi.amdsmi_get_processor_handles()[0]
+        m = amdsmi.amdsmi_get_gpu_metrics_info(_SMI["h"])
+        power = m.get("current_socket_power")
+        clocks = [c for c in (m.get("current_gfxclks") or []) if isinstance(c, int) and c > 0]
+        if not isinstance(power, (int, float)) or not clocks:
+            return None
+        return float(power), clocks
+    except Exception:
+        return None
+
+
+def sustained_clock(step, seconds: float):
+    """Run `step` back to back for `seconds` and sample power and clocks
+    from a second thread (after a 1 s ramp)."""
+    import statistics
+    import threading
+    import torch
+    stop = time.time() + seconds
+    samples = []
+
+    def sampler():
+        time.sleep(1.0)
+        while time.time() < stop - 0.5:
+            v = smi_sample()
+            if v:
+                samples.append(v)
+            time.sleep(0.3)
+
+    th = threading.Thread(target=sampler)
+    th.start()
+    while time.time() < stop:
+        for _ in range(10):
+            step(False)
+        torch.cuda.synchronize()
+    th.join()
+    if not samples:
+        return None
+    clk = statistics.median([c for _, cs in samples for c in cs])
+    return {"gfx_clock_mhz_median": clk, "socket_power_w_median": statistics.median([p for p, _ in samples]),
+            "samples": len(samples)}
+
+
 def cpu_baseline(target_s: float):
     """The oracle's fp64 GEMMs of the step (up and down projections) on a
     row sample sized for about target_s seconds (the whole GEMMs if the host
@@ -87,6 +139,93 @@ def cpu_baseline(target_s: float):
                       f"of X W_up and H W_down: {flops / 1e12:.3f} TFLOP in {t:.2f} s"}
 
 
+def compare_layouts(reps: int):
+    """Per-launch time of the same GEMM kernel under three operand layouts /
+    tile maps on the Llama FFN forward shapes: CCL operands with the
+    XCD-aware map (ccl_gemm), row-major operands with native dispatch, and
+    row-major operands with the XCD-aware map (ccl_gemm_rowmajor)."""
+    import numpy as np
+    import torch
+    from paper_2606_11718_amd import ccl
+
+    out = {}
+    for name, (M, N, K) in (("llama_up", (8192, 28672, 8192)), ("llama_down", (8192, 8192, 28672))):
+        plan = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+        g = torch.Generator(device="cuda").manual_seed(7)
+        A = (torch.randn(M * K, device="cuda", generator=g)).to(torch.bfloat16)
+        B = (torch.randn(K * N, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+        C = torch.empty(M * N, device="cuda", dtype=torch.bfloat16)
+        st = torch.cuda.current_stream()
+        variants = {
+            "ccl_remap": lambda: ccl.ccl_gemm(plan, A, B, C, st),
+            "rowmajor_native": lambda: ccl.ccl_gemm_rowmajor(plan, A, B, C, 0, st),
+            "rowmajor_remap": lambda: ccl.ccl_gemm_rowmajor(plan, A, B, C, 1, st),
+        }
+        res = {}
+        for vname, fn in variants.items():
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+                e0.record(st)
+                fn()
+                e1.record(st)
+                ts.append((e0, e1))
+            torch.cuda.synchronize()
+            ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
+            res[vname] = {"ms": round(ms, 4), "tflops": round(2 * M * N * K / ms / 1e9, 1)}
+        out[name] = res
+    return out
+
+
+def remote_report():
+    """Remote-byte model (the library's host model) for every workload GEMM,
+    grid and page size: totals per placement, floor, excess over the floor,
+    RR/CCL and COARSE/CCL ratios; geomean of best-of-grid ratios per model
+    family (best-of-grid: min over grids per placement, as the paper keeps
+    the best partition per placement)."""
+    import math
+    import workloads as W
+    from paper_2606_11718_amd import ccl
+
+    rows, best = [], {}
+    for wl in W.WORKLOADS.values():
+        for g in wl.gemms:
+            grids = g.grids if g.grids != (0,) else (0,)
+            for gr in grids:
+                for P in g.pages:
+                    plan = ccl.ccl_plan(g.M, g.N, g.K, g.chiplets, gr, P)
+                    Gr, Gc = ccl.ccl_plan_grid(plan)
+                    rec = {}
+                    for name, code in (("rr", ccl.CCL_PLACE_RR), ("coarse", ccl.CCL_PLACE_COARSE),
+                                       ("ccl", ccl.CCL_PLACE_CCL)):
+                        r = ccl.ccl_remote_bytes(plan, code, g.a_trans | (g.b_trans << 1))
+                        rec[name] = sum(r["remote"])
+                        rec["floor"] = r["floor"]
+                        rec["accessed"] = sum(r["accessed"])
+                    row = {"gemm": g.name, "MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{Gr}x{Gc}", "page": P,
+                           **rec, "excess_rr": rec["rr"] - rec["floor"], "excess_coarse": rec["coarse"] - rec["floor"],
+                           "excess_ccl": rec["ccl"] - rec["floor"],
+                           "rr_over_ccl": rec["rr"] / rec["ccl"] if rec["ccl"] else None,
+                           "coarse_over_ccl": rec["coarse"] / rec["ccl"] if rec["ccl"] else None}
+                    rows.append(row)
+                    key = (g.name, P)
+                    b = best.setdefault(key, {"rr": None, "coarse": None, "ccl": None})
+                    for pl in ("rr", "coarse", "ccl"):
+                        b[pl] = rec[pl] if b[pl] is None else min(b[pl], rec[pl])
+    fam = {"qwen": [], "llama": []}
+    for (name, P), b in best.items():
+        if P != 4096 or name == "tiny":
+            continue
+        fam["qwen" if name.startswith("qwen") else "llama"].append((b["rr"] / b["ccl"], b["coarse"] / b["ccl"]))
+    geo = {f: {"rr_over_ccl": math.exp(sum(math.log(x) for x, _ in v) / len(v)),
+               "coarse_over_ccl": math.exp(sum(math.log(y) for _, y in v) / len(v)), "gemms": len(v)}
+           for f, v in fam.items() if v}
+    return {"rows": rows, "best_of_grid_geomean_4k": geo}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -94,17 +233,32 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--remote-report", action="store_true",
+                    help="only print the remote-byte model report (host only, no GPU)")
+    ap.add_argument("--compare-layouts", action="store_true",
+                    help="only time CCL vs row-major operands and tile maps, print one JSON line")
+    ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--clock-seconds", type=float, default=4.0,
+                    help="sustained run after the timed steps that samples clock/power (0: off)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); the CCL GEMM "
               "path here has no multi-GPU sharding.", file=sys.stderr)
         sys.exit(2)
 
+    if args.remote_report:
+        print(json.dumps(remote_report()), flush=True)
+        return
+
     import numpy as np
     import torch
 
     import workloads as W
     from paper_2606_11718_amd import ccl
+
+    if args.compare_layouts:
+        print(json.dumps({"compare_layouts": compare_layouts(args.reps)}), flush=True)
+        return
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -217,7 +371,9 @@ def main():
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic, "kernel": "gemm_kernel<256,256> (up and down launches)",
+                     "traffic": traffic,
+                     "kernel": "gemm_kernel<256,256,%d waves> (up and down launches)" % (
+                         8 if ccl.ccl_debug_gemm_config(plan_up)[:2] == (256, 256) else 4),
                      "avg_launch_ms": round(gemm_ms, 4)},
         "kernels_ms": {k: round(v, 4) for k, v in avg.items()},
         "copy_roofline": {"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
@@ -225,6 +381,12 @@ def main():
                           "unpack_y": round(copy_bytes / (avg["unpack_y"] * 1e-3) / 1e9, 1)},
         "remote_bytes": remote,
     }
+    if args.clock_seconds > 0:
+        clk = sustained_clock(step, args.clock_seconds)
+        if clk:
+            clk["clock_adjusted_peak_tflops"] = round(PEAK_BF16_TFLOPS * clk["gfx_clock_mhz_median"] / 2400.0, 1)
+            clk["gemm_frac_of_clock_adjusted_peak"] = round(achieved / clk["clock_adjusted_peak_tflops"], 4)
+        out["sustained_clock"] = clk
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -142,11 +142,24 @@ ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void
  * so chiplets must divide 8.
  * Errors: CCL_ERR_INVALID_ARG (null pointer); CCL_ERR_MISALIGNED_POINTER
  * (pointer not 16-byte aligned); CCL_ERR_UNSUPPORTED (chiplets not dividing
- * 8, K / Gc or K / Gr not a multiple of 64, device not gfx950);
+ * 8, K / Gc or K / Gr not a multiple of 32, device not gfx950);
  * CCL_ERR_HIP.
  */
 ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
                     void* stream);
+
+/*
+ * Baseline for comparison with ccl_gemm (the layout the paper starts from,
+ * Sec. II-B Eq. 2): the same GEMM kernel on plain row-major operands
+ * A (M x K), B (K x N) and C (M x N), leading dimensions K, N and N, with
+ * the plan's tile grid. remap = 1 sends every tile to an XCD of the chiplet
+ * owning its partition, as ccl_gemm does; remap = 0 keeps the native
+ * dispatch order (workgroup w computes the w-th tile of a grouped raster
+ * over all of C and runs on XCD w mod 8, whoever owns the tile).
+ * Errors as ccl_gemm; CCL_ERR_INVALID_ARG also for remap not 0 or 1.
+ */
+ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void* C, int remap,
+                             void* stream);
 
 /*
  * Remote-byte record of the plan's GEMM under `placement` (Sec. IV-A).

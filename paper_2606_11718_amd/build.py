@@ -21,7 +21,7 @@ ARCH = "gfx950"
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU ops.
 # Code object v5: loadable by the HIP runtime bundled with torch (ROCm 7.0)
 # as well as by the system ROCm 7.2 runtime.
-HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-mcode-object-version=5",
+HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-inline-asm", "-mcode-object-version=5",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", CSRC]

@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 
 # every symbol include/ccl.h declares
 EXPORTED = ("ccl_plan", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
-            "ccl_unpack", "ccl_gemm", "ccl_remote_bytes", "ccl_status_string", "ccl_last_error",
+            "ccl_unpack", "ccl_gemm", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
@@ -73,6 +73,7 @@ def library() -> ctypes.CDLL:
         "ccl_pack": [vp, i32, vp, i64, i32, vp, vp],
         "ccl_unpack": [vp, i32, vp, vp, i64, vp],
         "ccl_gemm": [vp, vp, vp, vp, vp],
+        "ccl_gemm_rowmajor": [vp, vp, vp, vp, i32, vp],
         "ccl_remote_bytes": [vp, i32, i32, ctypes.POINTER(_Traffic)],
         "ccl_debug_tile_of_wg": [vp, i64, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "ccl_debug_gemm_config": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64)],
@@ -173,6 +174,10 @@ def ccl_unpack(plan: Plan, op: int, src_ccl, dst, ld: int, stream=None) -> None:
 
 def ccl_gemm(plan: Plan, A_ccl, B_ccl, C_ccl, stream=None) -> None:
     _check(library().ccl_gemm(plan, _ptr(A_ccl), _ptr(B_ccl), _ptr(C_ccl), _stream(stream)))
+
+
+def ccl_gemm_rowmajor(plan: Plan, A, B, C, remap: int, stream=None) -> None:
+    _check(library().ccl_gemm_rowmajor(plan, _ptr(A), _ptr(B), _ptr(C), remap, _stream(stream)))
 
 
 def ccl_remote_bytes(plan: Plan, placement: int, stored_trans_mask: int) -> dict:

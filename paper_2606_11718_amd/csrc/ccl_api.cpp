@@ -73,6 +73,23 @@ void ccl_addressing(const ccl::Plan& p, ccl::OperandAddr* a, ccl::OperandAddr* b
   *c = {p.Gc * sc, sc, (int32_t)(p.N / p.Gc), 0};
 }
 
+// Row-major addressing of the same operands (Eq. 2): A (M x K), B (K x N),
+// C (M x N), leading dimensions K, N, N.
+void rowmajor_addressing(const ccl::Plan& p, ccl::OperandAddr* a, ccl::OperandAddr* b,
+                         ccl::OperandAddr* c) {
+  const int64_t hr = p.M / p.Gr;
+  *a = {hr * p.K, p.K / p.Gc, (int32_t)p.K, (int32_t)(p.K / p.Gc)};
+  *b = {p.N / p.Gc, (p.K / p.Gr) * p.N, (int32_t)p.N, (int32_t)(p.K / p.Gr)};
+  *c = {hr * p.N, p.N / p.Gc, (int32_t)p.N, 0};
+}
+
+// The kernel addresses a tile's K step with 32-bit byte offsets from its
+// corner: up to 255 rows of A and 31 rows of B.
+bool offsets_fit(const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
+  const int64_t lim = ((int64_t)1 << 31) - 4096;
+  return 255 * (int64_t)a.ld * 2 < lim && 31 * (int64_t)b.ld * 2 < lim;
+}
+
 }  // namespace
 
 extern "C" {
@@ -157,10 +174,28 @@ ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void*
     return fail(CCL_ERR_MISALIGNED_POINTER, "A, B and C must be 16-byte aligned");
   const ccl::Plan& p = plan->plan;
   if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
-  if (ccl_status s = check_device()) return s;
   ccl::OperandAddr a, b, c;
   ccl_addressing(p, &a, &b, &c);
+  if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
+  if (ccl_status s = check_device()) return s;
   return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true,
+                                     static_cast<hipStream_t>(stream)),
+                    "gemm launch");
+}
+
+ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void* C, int remap,
+                             void* stream) {
+  if (!plan || !A || !B || !C) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (remap != 0 && remap != 1) return fail(CCL_ERR_INVALID_ARG, "remap must be 0 or 1");
+  if (!aligned16(A) || !aligned16(B) || !aligned16(C))
+    return fail(CCL_ERR_MISALIGNED_POINTER, "A, B and C must be 16-byte aligned");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  ccl::OperandAddr a, b, c;
+  rowmajor_addressing(p, &a, &b, &c);
+  if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "rows too long for 32-bit in-tile offsets");
+  if (ccl_status s = check_device()) return s;
+  return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1,
                                      static_cast<hipStream_t>(stream)),
                     "gemm launch");
 }

@@ -52,7 +52,7 @@ void choose_gemm_config(Plan* p) {
     return;
   }
   if ((p->K / p->Gc) % kGemmBK != 0 || (p->K / p->Gr) % kGemmBK != 0) {
-    g.why_unsupported = "K / grid_cols and K / grid_rows must be multiples of 64";
+    g.why_unsupported = "K / grid_cols and K / grid_rows must be multiples of 32";
     return;
   }
   g.xcd_per_chiplet = kNumXcd / p->G;
@@ -91,6 +91,11 @@ void choose_gemm_config(Plan* p) {
   int gm = 4;
   if (const char* e = std::getenv("CCL_GEMM_GROUP_M")) gm = std::max(1, std::atoi(e));
   g.group_m = (int)std::min<int64_t>(gm, g.tiles_m);
+  // 256x256 tiles run with 8 waves (two per SIMD) by default; CCL_GEMM_WAVES=4
+  // selects the 4-wave form of the same kernel.
+  g.waves = (btm == 256 && btn == 256) ? 8 : 4;
+  if (const char* e = std::getenv("CCL_GEMM_WAVES"))
+    g.waves = (std::atoi(e) == 8 && btm == 256 && btn == 256) ? 8 : 4;
   if (g.workgroups > 0x7fffffff) {
     g.why_unsupported = "launch too large";
     return;

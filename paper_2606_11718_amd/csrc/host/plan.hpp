@@ -14,7 +14,7 @@ constexpr int kModelTile = 128;   // output tile of the traffic model (Sec. IV-A
 constexpr int kElemBytes = 2;     // bf16
 constexpr int kNumXcd = 8;        // MI355X: 8 XCDs, workgroups dispatched round-robin
 constexpr int kMaxChiplets = 64;
-constexpr int kGemmBK = 64;       // K extent of one GEMM main-loop step
+constexpr int kGemmBK = 32;       // K extent of one GEMM main-loop step
 
 enum Op { OP_A = 0, OP_B = 1, OP_C = 2 };
 enum Placement { PLACE_RR = 0, PLACE_COARSE = 1, PLACE_CCL = 2 };
@@ -40,6 +40,7 @@ struct GemmConfig {
   int64_t tiles_per_xcd = 0;        // ceil(tiles per partition / xcd_per_chiplet)
   int64_t workgroups = 0;           // 8 * tiles_per_xcd
   int group_m = 0;                  // raster group height (tiles) inside a partition
+  int waves = 4;                    // waves per workgroup (8 only for 256x256)
   bool supported = false;           // whether ccl_gemm can run this plan
   std::string why_unsupported;
 };

@@ -36,8 +36,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
-constexpr int kBK = 64;
-constexpr int kThreads = 256;
+constexpr int kBK = 32;          // K extent of one main-loop step
+constexpr int kStages = 4;       // LDS stages; loads run kStages-1 steps ahead
 
 struct GemmParams {
   const uint16_t* A;
@@ -45,15 +45,18 @@ struct GemmParams {
   uint16_t* C;
   OperandAddr a, b, c;
   TileMap map;
-  int32_t ksteps;       // K / 64
+  int32_t ksteps;       // K / 32
   int32_t remap;        // 1: XCD-aware map; 0: native raster over the whole C
   int32_t grid_r;       // Gr (native raster)
 };
 
 // LDS chunk swizzles (16-byte chunk index XOR a function of the row).
-// A rows are 128 B (8 chunks): rows r..r+15 read at one logical chunk land
-// on 16 distinct (row parity, slot) pairs.
-__device__ __forceinline__ int swz_a(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+// A rows are 64 B (4 chunks): chunk slot = logical chunk XOR (row / 4) mod 4,
+// so the 16 rows a quarter-wave reads at one logical chunk fill all 16
+// 16-byte columns of a 256-byte bank row. (Measured on gfx950 with
+// SQ_LDS_BANK_CONFLICT: zero conflicts for this form, while e.g. row mod 4
+// or (row / 2) mod 4 give 2- to 4-way conflicts.)
+__device__ __forceinline__ int swz_a(int row) { return (row >> 2) & 3; }
 // B rows are BN*2 bytes: the 4 rows one 16-lane transpose read touches get
 // disjoint 32-byte (and 64-byte) bank windows.
 __device__ __forceinline__ int swz_b(int row) { return ((row & 3) << 1) ^ ((row & 3) << 2); }
@@ -64,42 +67,81 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return u >> 16;
 }
 
-__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char;
 
-template <int BM, int BN>
+// Raw buffer descriptor (stride 0): `num_records` bytes from `base`; a load
+// at offset >= num_records returns zero without touching memory.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int32_t num_records) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = (int)(uint32_t)a;
+  r[1] = (int)((a >> 32) & 0xffffu);
+  r[2] = num_records;
+  r[3] = 0x00020000;
+  return r;
+}
+
+// 16 bytes per lane from the buffer straight into LDS at `lds` + 16*lane.
+// Written as inline assembly so that the compiler does not track these LDS
+// writes itself: it cannot tell the stage arrays apart and would wait for
+// loads of later stages before reading the current one. The kernel orders
+// them with explicit vmcnt waits and barriers; nothing else in it uses M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t voff, const char* lds) {
+  const uint32_t m0v = (uint32_t)(uintptr_t)(const lds_char*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(m0v), "v"(voff), "s"(rsrc) : "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt immediate: vmcnt(vm) and lgkmcnt(lgkm), expcnt not waited on.
+constexpr int waitcnt_imm(int vm, int lgkm) {
+  return (vm & 15) | (7 << 4) | ((lgkm & 15) << 8) | (((vm >> 4) & 3) << 14);
+}
+
+// Output tile BM x BN computed by a 2 x WGN grid of waves.
+template <int BM, int BN, int WGN>
 struct Tile {
-  static constexpr int WM = BM / 2, WN = BN / 2;       // wave tile
+  static constexpr int NW = 2 * WGN;                   // waves per workgroup
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;     // wave tile
   static constexpr int TM = WM / 32, TN = WN / 32;     // MFMA tiles per wave
-  static constexpr int A_BYTES = BM * kBK * 2;
+  static constexpr int A_BYTES = BM * kBK * 2;         // one stage
   static constexpr int B_BYTES = kBK * BN * 2;
-  static constexpr int NA = BM / 32;                   // A load instructions per wave per stage
+  static constexpr int NA = BM / (16 * NW);            // A loads per wave per stage (1 KB each)
   static constexpr int CPR_B = BN / 8;                 // 16-byte chunks per B row
   static constexpr int RPI_B = 64 / CPR_B;             // B rows per load instruction
-  static constexpr int NB = BN / 32;                   // B load instructions per wave per stage
+  static constexpr int NB = BN / (16 * NW);            // B loads per wave per stage
+  static constexpr int NL = NA + NB;
+  static_assert(NA >= 1 && NB >= 1 && TN >= 1, "tile too small for the wave grid");
 };
 
-// MFMA operand fragments of one kk sub-step: A rows and B columns.
+// MFMA operand fragments of one 16-wide kk sub-step: A rows and B columns.
 template <int TM, int TN>
 struct FragSet {
   bf16x8 a[TM];
-  bf16x8 b[TN];
+  i16x4 b[TN][2];     // two transposed halves (k 0..3 and 4..7) per B fragment
 };
 
-// Instruction classes for __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008;
-constexpr int kSchedVmemRead = 0x020;
-constexpr int kSchedDsRead = 0x100;
-
-template <int BM, int BN>
-__global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
+template <int BM, int BN, int WGN>
+__global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) {
   // The host pass only needs the launch stub; the body uses device-only
   // buffer-resource builtins.
 #if defined(__HIP_DEVICE_COMPILE__)
-  using T = Tile<BM, BN>;
+  using T = Tile<BM, BN, WGN>;
+  // One array per stage, so that the compiler tracks the direct-to-LDS
+  // writes of each stage separately.
   __shared__ __attribute__((aligned(1024))) char smA0[T::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char smA1[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smA2[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smA3[T::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char smB0[T::B_BYTES];
   __shared__ __attribute__((aligned(1024))) char smB1[T::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB2[T::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
+  static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
 
   int32_t pr, pc, ti, tj;
   if (p.remap) {
@@ -123,14 +165,15 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
   // ---- global -> LDS: per-lane byte offsets from the K step's tile corner ----
+  // A load i of this wave fills LDS rows 16*(wave*NA+i) .. +15 (64 B each).
   uint32_t a_voff[T::NA];
 #pragma unroll
   for (int i = 0; i < T::NA; ++i) {
-    const int row = 8 * (wave * T::NA + i) + (lane >> 3);
-    const int chunk = (lane & 7) ^ swz_a(row);
+    const int row = 16 * (wave * T::NA + i) + (lane >> 2);
+    const int chunk = (lane & 3) ^ swz_a(row);
     a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
   }
   uint32_t b_voff[T::NB];
@@ -145,12 +188,12 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
   const int32_t b_extent = (kBK - 1) * p.b.ld * 2 + BN * 2;
 
   // ---- LDS fragment read offsets (bytes) ----
-  int32_t a_rd[4];
+  int32_t a_rd[2];
   {
     const int row = wm * T::WM + (lane & 31);
     const int h = lane >> 5;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) a_rd[kk] = row * 128 + (((2 * kk + h) ^ swz_a(row)) * 16);
+    for (int kk = 0; kk < 2; ++kk) a_rd[kk] = row * 64 + (((2 * kk + h) ^ swz_a(row)) * 16);
   }
   int32_t b_rd[T::TN][2];
   {
@@ -172,25 +215,18 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
   int64_t a_slice_off = 0, b_slice_off = 0;
   int32_t a_kl = 0, b_kl = 0;
 
-  // Issue the direct-to-LDS loads of the next K step. With live == false
-  // the descriptors cover zero bytes: every load is out of range, touches
-  // no memory and writes zeros to the (unused) stage.
-  auto load_stage = [&](char* smA, char* smB, bool live) {
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a_base + a_slice_off + a_kl), (short)0, live ? a_extent : 0, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(b_base + b_slice_off + (int64_t)b_kl * p.b.ld), (short)0, live ? b_extent : 0,
-        0x00020000);
-#pragma unroll
-    for (int i = 0; i < T::NA; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(smA + (wave * T::NA + i) * 1024), 16,
-                                               a_voff[i], 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < T::NB; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(smB + (wave * T::NB + i) * 1024), 16,
-                                               b_voff[i], 0, 0, 0);
+  // Descriptors of the next K step to be loaded. With live == false they
+  // cover zero bytes: every load is out of range, touches no memory and
+  // writes zeros to the (unused) stage.
+  struct StageSrc {
+    i32x4 ra, rb;
+  };
+  auto next_src = [&](bool live) {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_base + a_slice_off + a_kl, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_base + b_slice_off + (int64_t)b_kl * p.b.ld, live ? b_extent : 0);
     // advance to the next K step (branch-free; past the last step the
-    // corners are never used with a non-empty descriptor)
+    // corners are only used with empty descriptors)
     a_kl += kBK;
     const bool a_wrap = a_kl == p.a.kslice;
     a_kl = a_wrap ? 0 : a_kl;
@@ -199,21 +235,36 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
     const bool b_wrap = b_kl == p.b.kslice;
     b_kl = b_wrap ? 0 : b_kl;
     b_slice_off += b_wrap ? p.b.slice : 0;
+    return d;
+  };
+  // Load i (0 .. NL-1) of this wave for one stage.
+  auto load_one = [&](const StageSrc& d, char* smA, char* smB, int i) {
+    if (i < T::NA)
+      lds_dma16(d.ra, a_voff[i], smA + (wave * T::NA + i) * 1024);
+    else
+      lds_dma16(d.rb, b_voff[i - T::NA], smB + (wave * T::NB + (i - T::NA)) * 1024);
+  };
+  auto load_stage = [&](char* smA, char* smB, bool live) {
+    const StageSrc d = next_src(live);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d, smA, smB, i);
   };
 
   using Frags = FragSet<T::TM, T::TN>;
+  constexpr int kReadsPerKK = T::TM + 2 * T::TN;
+  // LDS read i (0 .. kReadsPerKK-1) of the kk sub-step's fragments.
+  auto read_one = [&](const char* smA, const char* smB, int kk, Frags& f, int i) {
+    if (i < T::TM) {
+      f.a[i] = *(const lds_bf16x8*)(smA + a_rd[kk] + i * 32 * 64);
+    } else {
+      const int nt = (i - T::TM) >> 1, r = (i - T::TM) & 1;
+      f.b[nt][r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(smB + b_rd[nt][r] + kk * 16 * BN * 2));
+    }
+  };
   auto read_frags = [&](const char* smA, const char* smB, int kk, Frags& f) {
 #pragma unroll
-    for (int mt = 0; mt < T::TM; ++mt)
-      f.a[mt] = *(const lds_bf16x8*)(smA + a_rd[kk] + mt * 32 * 128);
-#pragma unroll
-    for (int nt = 0; nt < T::TN; ++nt) {
-      i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(smB + b_rd[nt][0] + kk * 16 * BN * 2));
-      i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(smB + b_rd[nt][1] + kk * 16 * BN * 2));
-      f.b[nt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    }
+    for (int i = 0; i < kReadsPerKK; ++i) read_one(smA, smB, kk, f, i);
   };
 
   f32x16 acc[T::TM][T::TN];
@@ -224,63 +275,69 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto mfmas = [&](const Frags& f) {
-#pragma unroll
-    for (int mt = 0; mt < T::TM; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < T::TN; ++nt)
-        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[nt], f.a[mt], acc[mt][nt], 0, 0, 0);
-  };
-
   constexpr int kMfmaPerKK = T::TM * T::TN;
-  constexpr int kReadsPerKK = T::TM + 2 * T::TN;
-  // Behind each MFMA issue at most one buffer load and one LDS read, so the
-  // matrix pipe stays fed while the memory instructions drain.
-  auto interleave = [&](int n_vmem) {
+  auto mfma_one = [&](const Frags& f, int i) {
+    const int mt = i / T::TN, nt = i % T::TN;
+    const bf16x8 b = __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(f.b[nt][0], f.b[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
+    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, f.a[mt], acc[mt][nt], 0, 0, 0);
+  };
+  // One kk sub-step: MFMAs on f, each followed by at most one direct-to-LDS
+  // load of a later stage (when d is given) and one LDS read of the next
+  // fragments into g. The order is pinned so the matrix pipe always has
+  // the next MFMA ready while the memory instructions drain behind it.
+  auto substep = [&](const Frags& f, const StageSrc* d, char* lA, char* lB, const char* rA,
+                     const char* rB, int rkk, Frags& g) {
 #pragma unroll
     for (int i = 0; i < kMfmaPerKK; ++i) {
-      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-      if (i < n_vmem) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
-      if (i < kReadsPerKK) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+      mfma_one(f, i);
+      if (d && i < T::NL) load_one(*d, lA, lB, i);
+      if (i < kReadsPerKK) read_one(rA, rB, rkk, g, i);
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
-    for (int i = kMfmaPerKK; i < n_vmem; ++i) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+    for (int i = kMfmaPerKK; i < kReadsPerKK; ++i) read_one(rA, rB, rkk, g, i);
 #pragma unroll
-    for (int i = kMfmaPerKK; i < kReadsPerKK; ++i) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+    for (int i = kMfmaPerKK; i < T::NL; ++i)
+      if (d) load_one(*d, lA, lB, i);
     __builtin_amdgcn_sched_barrier(0);
   };
 
+  // Wait for the own loads of the next stage (the later stages' loads stay
+  // in flight), then for every wave: after this barrier the next stage is
+  // complete in LDS, and nobody reads the stage that the next load reuses.
+  // An LDS-only wait: a full fence would also wait for the in-flight
+  // direct-to-LDS loads of the later stages.
+  auto stage_barrier = [&]() {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * T::NL, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
   Frags f0, f1;
-  // One K step on LDS stage (smA, smB), whose kk = 0 fragments are in f0.
-  // The next step's loads go to (nA, nB) (dummy when !live) and its kk = 0
-  // fragments are read into f0 at the end.
-  auto step = [&](const char* smA, const char* smB, char* nA, char* nB, bool live) {
-    load_stage(nA, nB, live);
-    read_frags(smA, smB, 1, f1);
-    mfmas(f0);
-    interleave(T::NA + T::NB);
-    read_frags(smA, smB, 2, f0);
-    mfmas(f1);
-    interleave(0);
-    read_frags(smA, smB, 3, f1);
-    mfmas(f0);
-    interleave(0);
-    // all of this stage is in registers; the next stage's loads must land
-    wait_vm_all();
-    __syncthreads();
-    read_frags(nA, nB, 0, f0);
-    mfmas(f1);
-    interleave(0);
+  // One K step on stage (smA, smB), whose kk = 0 fragments are in f0. The
+  // step kStages-1 ahead is loaded into (lA, lB); the next stage (nA, nB)
+  // is waited for, and its kk = 0 fragments are read into f0.
+  auto step = [&](const char* smA, const char* smB, char* lA, char* lB, const char* nA,
+                  const char* nB, bool live) {
+    const StageSrc d = next_src(live);
+    substep(f0, &d, lA, lB, smA, smB, 1, f1);
+    stage_barrier();
+    substep(f1, nullptr, lA, lB, nA, nB, 0, f0);
   };
 
   const int32_t ksteps = p.ksteps;
-  load_stage(smA0, smB0, true);
-  wait_vm_all();
-  __syncthreads();
+  load_stage(smA0, smB0, 0 < ksteps);
+  load_stage(smA1, smB1, 1 < ksteps);
+  load_stage(smA2, smB2, 2 < ksteps);
+  stage_barrier();
   read_frags(smA0, smB0, 0, f0);
-  for (int32_t s = 0; s < ksteps; s += 2) {
-    step(smA0, smB0, smA1, smB1, s + 1 < ksteps);
-    if (s + 1 < ksteps) step(smA1, smB1, smA0, smB0, s + 2 < ksteps);
+  for (int32_t s = 0; s < ksteps; s += kStages) {
+    step(smA0, smB0, smA3, smB3, smA1, smB1, s + 3 < ksteps);
+    if (s + 1 < ksteps) step(smA1, smB1, smA0, smB0, smA2, smB2, s + 4 < ksteps);
+    if (s + 2 < ksteps) step(smA2, smB2, smA1, smB1, smA3, smB3, s + 5 < ksteps);
+    if (s + 3 < ksteps) step(smA3, smB3, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
   // ---- epilogue: lane holds C[m][n .. n+3] for each (mt, nt, q) ----
@@ -340,17 +397,24 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   gp.grid_r = p.Gr;
   const unsigned wgs = remap ? (unsigned)g.workgroups
                              : (unsigned)(g.tiles_m * g.tiles_n * p.G);
-  dim3 grid(wgs), block(kThreads);
-  if (g.tile_m == 256 && g.tile_n == 256)
-    hipLaunchKernelGGL((gemm_kernel<256, 256>), grid, block, 0, stream, gp);
+  dim3 grid(wgs);
+  const int waves = g.waves;
+#define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
+  hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \
+                     stream, gp)
+  if (g.tile_m == 256 && g.tile_n == 256 && waves == 8)
+    CCL_LAUNCH(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 256)
+    CCL_LAUNCH(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128)
-    hipLaunchKernelGGL((gemm_kernel<256, 128>), grid, block, 0, stream, gp);
+    CCL_LAUNCH(256, 128, 2);
   else if (g.tile_m == 128 && g.tile_n == 256)
-    hipLaunchKernelGGL((gemm_kernel<128, 256>), grid, block, 0, stream, gp);
+    CCL_LAUNCH(128, 256, 2);
   else if (g.tile_m == 128 && g.tile_n == 128)
-    hipLaunchKernelGGL((gemm_kernel<128, 128>), grid, block, 0, stream, gp);
+    CCL_LAUNCH(128, 128, 2);
   else
     return hipErrorInvalidValue;
+#undef CCL_LAUNCH
   return hipGetLastError();
 }
 

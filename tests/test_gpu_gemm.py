@@ -21,16 +21,20 @@ from tests.helpers import CANARY, dev_full, from_dev, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None, unpack=True):
+def run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None, unpack=True,
+             waves=None):
     """Pack A and B on the GPU and run the GEMM. Returns (C, plan) where C is
     the row-major bf16 bits (oracle unpack), or (ccl buffer, Gr, Gc) when
-    unpack is False."""
+    unpack is False. tile / waves force the kernel variant."""
     if tile:
         os.environ["CCL_GEMM_TILE"] = tile
+    if waves:
+        os.environ["CCL_GEMM_WAVES"] = str(waves)
     try:
         plan = ccl.ccl_plan(M, N, K, G, Gr, P)
     finally:
         os.environ.pop("CCL_GEMM_TILE", None)
+        os.environ.pop("CCL_GEMM_WAVES", None)
     gr, gc = ccl.ccl_plan_grid(plan)
     tm_, tn_, wgs = ccl.ccl_debug_gemm_config(plan)
     print(f"gemm {M}x{N}x{K} grid {gr}x{gc} P={P} tile {tm_}x{tn_} wgs={wgs} "
@@ -52,8 +56,8 @@ def _logical(stored, trans):
     return np.ascontiguousarray(stored.T) if trans else stored
 
 
-def _check_full(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None):
-    Cbits, _ = run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile)
+def _check_full(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile=None, waves=None):
+    Cbits, _ = run_gemm(A_stored, a_trans, B_stored, b_trans, M, N, K, G, Gr, P, tile, waves=waves)
     C_ref = OG.gemm_fp64(_logical(A_stored, a_trans), _logical(B_stored, b_trans))
     err = OG.errors(OG.decode_bf16(Cbits), C_ref)
     print("errors", err, flush=True)
@@ -77,12 +81,14 @@ def test_qwen_backward_grids_are_the_automatic_choice():
         assert ccl.ccl_plan_grid(p)[0] == expect == OP.auto_grid_rows(g.M, g.N, g.K, g.chiplets)
 
 
-@pytest.mark.parametrize("tile", ["256x256", "256x128", "128x256", "128x128"])
-def test_gemm_every_kernel_tile(tile):
-    M, N, K = 2048, 2048, 1024
+@pytest.mark.parametrize("tile,waves", [("256x256", 8), ("256x256", 4), ("256x128", 4),
+                                        ("128x256", 4), ("128x128", 4)])
+@pytest.mark.parametrize("M,N,K,G,Gr", [(2048, 2048, 1024, 8, 2),      # 2x4 grid, 32 K steps
+                                        (1024, 1024, 1056, 1, 1)])     # 33 K steps: ragged stage ring
+def test_gemm_every_kernel_variant(tile, waves, M, N, K, G, Gr):
     A = W.draw_array(901, M, K, "normal", 1.0)
     B = W.draw_array(902, K, N, "normal", 0.02)
-    _check_full(A, 0, B, 0, M, N, K, 8, 2, 4096, tile)
+    _check_full(A, 0, B, 0, M, N, K, G, Gr, 4096, tile, waves)
 
 
 @pytest.mark.parametrize("M,N,K,G,Gr,P,ta,tb", [
@@ -176,3 +182,20 @@ def test_dispatch_probe_tiles_run_on_owner_xcd(M, N, K, G, Gr):
     for xcd, ti, tj, owner in live:
         assert owner == OP.owner(ti * tm_ // 128, tj * tn_ // 128, M, N, Gr, G // Gr)
         assert xcd in OP.xcds_of_chiplet(owner, G)
+
+
+@pytest.mark.parametrize("remap", [0, 1])
+@pytest.mark.parametrize("M,N,K,G,Gr", [(2048, 3072, 1024, 8, 2), (1024, 1024, 512, 8, 8),
+                                        (256, 512, 256, 4, 2)])
+def test_gemm_rowmajor_baseline(remap, M, N, K, G, Gr):
+    """The comparison baseline: the same kernel on plain row-major operands,
+    with (remap=1) or without (remap=0) the XCD-aware tile map."""
+    A = W.draw_array(61 + M, M, K, "normal", 1.0)
+    B = W.draw_array(62 + N, K, N, "normal", 0.05)
+    plan = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+    C = dev_full(M * N)
+    print(f"rowmajor {M}x{N}x{K} grid {Gr}x{G // Gr} remap={remap}", flush=True)
+    ccl.ccl_gemm_rowmajor(plan, to_dev(A), to_dev(B), C, remap)
+    got = OG.decode_bf16(from_dev(C).reshape(M, N))
+    err = OG.errors(got, OG.gemm_fp64(A, B))
+    assert OG.within_tolerance(err), err

@@ -79,8 +79,10 @@ def test_null_arguments_are_rejected_without_gpu():
     assert lib.ccl_pack(p, 2, 16, 512, 1, 16, None) == 1     # C has no transpose
     assert lib.ccl_pack(p, 0, 16, 100, 0, 16, None) == 1     # ld < cols
     assert lib.ccl_unpack(p, 1, 16, 16, 10, None) == 1
+    assert lib.ccl_gemm_rowmajor(p, 16, 16, 16, 2, None) == 1    # remap must be 0/1
+    assert lib.ccl_gemm_rowmajor(p, 16, 32, 8, 1, None) == 4     # misaligned
     assert lib.ccl_plan_destroy(None) == 0
-    q = ccl.ccl_plan(256, 512, 192, 4, 2, 4096)             # K / Gc = 96: no GEMM kernel
+    q = ccl.ccl_plan(256, 512, 208, 4, 2, 4096)             # K / Gc = 104: no GEMM kernel
     with pytest.raises(ccl.CCLError) as ei:
         ccl.ccl_gemm(q, 16, 16, 16)
     assert ei.value.status == 3
