@@ -18,6 +18,10 @@ namespace ccl {
 
 namespace {
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte chunk
+
+constexpr int64_t kInfinityCacheBytes = 256ll << 20;          // MI355X MALL
+
 // q / d for q < 2^31, d < 2^31: multiply by ceil(2^s / d), s = 31 + ceil(log2 d).
 struct DivMagic {
   uint64_t mul;
@@ -52,9 +56,23 @@ struct PackArgs {
   DivMagic units_per_row;    // wc / V
 };
 
+// Load / store one unit; NT = non-temporal (streaming) access.
+template <bool NT, typename T>
+__device__ __forceinline__ T ld(const T* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <bool NT, typename T>
+__device__ __forceinline__ void st(T* p, T v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
 // V = elements per unit (8: one 16-byte vector, 1: one element).
 // UNPACK = false: row-major -> CCL; true: CCL -> row-major.
-template <int V, bool UNPACK>
+// NT: streaming accesses, used for tensors larger than the 256 MiB
+// Infinity Cache (measured: +10 % on a 470 MB copy, -15 % on a 134 MB one).
+template <int V, bool UNPACK, bool NT>
 __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
   const int32_t b = blockIdx.y;                      // strip / chiplet
   const int64_t pr = b / a.grid_c, pc = b % a.grid_c;
@@ -64,7 +82,7 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
   constexpr int UNROLL = 4;
   const uint32_t stride = gridDim.x * 256u;
   for (uint32_t base = blockIdx.x * 256u * UNROLL; base < a.units_per_block; base += stride * UNROLL) {
-    using T = typename std::conditional<V == 8, uint4, uint16_t>::type;
+    using T = typename std::conditional<V == 8, u32x4, uint16_t>::type;
     T v[UNROLL];
     int64_t rm_off[UNROLL];
     bool ok[UNROLL];
@@ -77,9 +95,9 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       rm_off[u] = (int64_t)row * a.ld + col;
       if (ok[u]) {
         if (UNPACK)
-          v[u] = *reinterpret_cast<const T*>(a.ccl + strip_base + (int64_t)q * V);
+          v[u] = ld<NT>(reinterpret_cast<const T*>(a.ccl + strip_base + (int64_t)q * V));
         else
-          v[u] = *reinterpret_cast<const T*>(src_rm + rm_off[u]);
+          v[u] = ld<NT>(reinterpret_cast<const T*>(src_rm + rm_off[u]));
       }
     }
 #pragma unroll
@@ -87,9 +105,9 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       const uint32_t q = base + threadIdx.x + u * 256u;
       if (ok[u]) {
         if (UNPACK)
-          *reinterpret_cast<T*>(dst_rm + rm_off[u]) = v[u];
+          st<NT>(reinterpret_cast<T*>(dst_rm + rm_off[u]), v[u]);
         else
-          *reinterpret_cast<T*>(a.ccl_out + strip_base + (int64_t)q * V) = v[u];
+          st<NT>(reinterpret_cast<T*>(a.ccl_out + strip_base + (int64_t)q * V), v[u]);
       }
     }
   }
@@ -183,17 +201,16 @@ hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, 
   a.units_per_block = (uint32_t)(L.block_rows * L.block_cols / V);
   a.units_per_row = make_div((uint32_t)(L.block_cols / V));
   dim3 grid(grid_x_for(a.units_per_block, 4), (unsigned)(L.grid_r * L.grid_c));
+  const bool nt = L.rows * L.cols * 2 > kInfinityCacheBytes;
+#define CCL_COPY(V_, U_, NT_) hipLaunchKernelGGL((copy_kernel<V_, U_, NT_>), grid, dim3(256), 0, stream, a)
   if (vec) {
-    if (unpack)
-      hipLaunchKernelGGL((copy_kernel<8, true>), grid, dim3(256), 0, stream, a);
-    else
-      hipLaunchKernelGGL((copy_kernel<8, false>), grid, dim3(256), 0, stream, a);
+    if (unpack) { if (nt) CCL_COPY(8, true, true); else CCL_COPY(8, true, false); }
+    else        { if (nt) CCL_COPY(8, false, true); else CCL_COPY(8, false, false); }
   } else {
-    if (unpack)
-      hipLaunchKernelGGL((copy_kernel<1, true>), grid, dim3(256), 0, stream, a);
-    else
-      hipLaunchKernelGGL((copy_kernel<1, false>), grid, dim3(256), 0, stream, a);
+    if (unpack) CCL_COPY(1, true, false);
+    else        CCL_COPY(1, false, false);
   }
+#undef CCL_COPY
   return hipGetLastError();
 }
 
