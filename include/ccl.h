@@ -170,6 +170,52 @@ ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void
 ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
                             ccl_traffic* out);
 
+/* Private L2 of each chiplet for ccl_remote_bytes_l2 (Sec. IV-A: the
+ * paper's configuration is 8 MB, 128-byte lines, 16-way per chiplet). */
+typedef struct {
+  int64_t l2_bytes;   /* capacity per chiplet; 0 = no cache. Otherwise a power-of-two
+                         number of sets of ways * line_bytes, and l2_bytes / line_bytes <= 2^24 */
+  int32_t ways;       /* associativity, >= 1 */
+  int32_t line_bytes; /* power of two, 16 .. page_bytes */
+  int32_t slots;      /* tiles a chiplet runs at once (its CTA concurrency), >= 1 */
+  int32_t k_step;     /* K elements every resident tile reads per step, >= 1 */
+  int32_t traversal;  /* order of a chiplet's tiles: 0 tile rows outer, 1 tile columns outer */
+  int32_t threads;    /* host threads; 0 = one per chiplet, up to the core count */
+} ccl_l2_config;
+
+/* Result of ccl_remote_bytes_l2. Index [0]=A, [1]=B, [2]=C. */
+typedef struct {
+  uint64_t accesses[2];          /* L2 line accesses of A and B */
+  uint64_t misses[2];            /* of which missed */
+  uint64_t remote[3];            /* bytes: remote misses * line_bytes (A, B); C lines written
+                                    to another chiplet * line_bytes */
+  uint64_t remote_per_chiplet[CCL_MAX_CHIPLETS];  /* charged to the chiplet running the tile */
+  int32_t chiplets;
+} ccl_l2_traffic;
+
+/*
+ * Remote-HBM traffic of the plan's GEMM with a private set-associative LRU L2
+ * per chiplet (Sec. IV-A simulation framework and metric; Fig. 7 sweeps the
+ * capacity). Model:
+ *   - chiplet p runs the 128x128 tiles of its partition in `traversal` order,
+ *     `slots` at a time; the tiles of such a wave step through K together,
+ *     k_step at a time, and at each step each tile (in wave order) reads the
+ *     lines of its A slice (128 x k_step) and then of its B slice
+ *     (k_step x 128), each in increasing address order of the operand as
+ *     stored (row-major, stored transposed per stored_trans_mask, or CCL);
+ *   - A is at address 0, B at 2^40, C at 2^41; a line's set is its line
+ *     number XOR-folded into log2(sets) bits; replacement is LRU;
+ *   - a miss is remote when the line's home chiplet under `placement` (as in
+ *     ccl_remote_bytes) is not p; after a wave, its C tiles are written
+ *     without allocating in L2, and every C line homed elsewhere counts.
+ * With l2_bytes = 0 and line-aligned slices the result equals
+ * ccl_remote_bytes. Host-only, synchronous; runs one host thread per chiplet.
+ * Errors: CCL_ERR_INVALID_ARG (NULL argument, bad placement or mask,
+ * invalid configuration).
+ */
+ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+                               const ccl_l2_config* config, ccl_l2_traffic* out);
+
 /* Static name of a status code. */
 const char* ccl_status_string(ccl_status status);
 

@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 
 # every symbol include/ccl.h declares
 EXPORTED = ("ccl_plan", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
-            "ccl_unpack", "ccl_gemm", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_status_string", "ccl_last_error",
+            "ccl_unpack", "ccl_gemm", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
@@ -44,6 +44,18 @@ class _Layout(ctypes.Structure):
 class _Traffic(ctypes.Structure):
     _fields_ = [("accessed", ctypes.c_uint64 * 3), ("remote", ctypes.c_uint64 * 3),
                 ("floor_bytes", ctypes.c_uint64), ("footprint", ctypes.c_uint64 * 3),
+                ("remote_per_chiplet", ctypes.c_uint64 * MAX_CHIPLETS), ("chiplets", ctypes.c_int32)]
+
+
+class _L2Config(ctypes.Structure):
+    _fields_ = [("l2_bytes", ctypes.c_int64), ("ways", ctypes.c_int32), ("line_bytes", ctypes.c_int32),
+                ("slots", ctypes.c_int32), ("k_step", ctypes.c_int32), ("traversal", ctypes.c_int32),
+                ("threads", ctypes.c_int32)]
+
+
+class _L2Traffic(ctypes.Structure):
+    _fields_ = [("accesses", ctypes.c_uint64 * 2), ("misses", ctypes.c_uint64 * 2),
+                ("remote", ctypes.c_uint64 * 3),
                 ("remote_per_chiplet", ctypes.c_uint64 * MAX_CHIPLETS), ("chiplets", ctypes.c_int32)]
 
 
@@ -75,6 +87,7 @@ def library() -> ctypes.CDLL:
         "ccl_gemm": [vp, vp, vp, vp, vp],
         "ccl_gemm_rowmajor": [vp, vp, vp, vp, i32, vp],
         "ccl_remote_bytes": [vp, i32, i32, ctypes.POINTER(_Traffic)],
+        "ccl_remote_bytes_l2": [vp, i32, i32, ctypes.POINTER(_L2Config), ctypes.POINTER(_L2Traffic)],
         "ccl_debug_tile_of_wg": [vp, i64, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "ccl_debug_gemm_config": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64)],
         "ccl_debug_dispatch": [vp, vp, vp],
@@ -189,6 +202,21 @@ def ccl_remote_bytes(plan: Plan, placement: int, stored_trans_mask: int) -> dict
         "remote_per_chiplet": list(t.remote_per_chiplet[:t.chiplets]),
         "floor": int(t.floor_bytes),
         "footprint": list(t.footprint),
+    }
+
+
+def ccl_remote_bytes_l2(plan: Plan, placement: int, stored_trans_mask: int, *, l2_bytes: int,
+                        slots: int, ways: int = 16, line_bytes: int = 128, k_step: int = 64,
+                        traversal: int = 0, threads: int = 0) -> dict:
+    cfg = _L2Config(l2_bytes, ways, line_bytes, slots, k_step, traversal, threads)
+    t = _L2Traffic()
+    _check(library().ccl_remote_bytes_l2(plan, placement, stored_trans_mask, ctypes.byref(cfg),
+                                         ctypes.byref(t)))
+    return {
+        "accesses": list(t.accesses),
+        "misses": list(t.misses),
+        "remote": list(t.remote),
+        "remote_per_chiplet": list(t.remote_per_chiplet[:t.chiplets]),
     }
 
 

@@ -4,10 +4,12 @@
 #include <cstdint>
 #include <cstring>
 #include <mutex>
+#include <exception>
 #include <new>
 #include <string>
 
 #include "../../include/ccl.h"
+#include "host/l2sim.hpp"
 #include "host/plan.hpp"
 #include "kernels/kernels.hpp"
 
@@ -215,6 +217,41 @@ ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored
     out->footprint[i] = t.footprint[i];
   }
   out->floor_bytes = t.floor_bytes;
+  for (int i = 0; i < t.chiplets; ++i) out->remote_per_chiplet[i] = t.remote_per_chiplet[i];
+  out->chiplets = t.chiplets;
+  return ok();
+}
+
+ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+                               const ccl_l2_config* config, ccl_l2_traffic* out) {
+  if (!plan || !config || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  if (placement != CCL_PLACE_RR && placement != CCL_PLACE_COARSE && placement != CCL_PLACE_CCL)
+    return fail(CCL_ERR_INVALID_ARG, "unknown placement");
+  if (stored_trans_mask < 0 || stored_trans_mask > 3)
+    return fail(CCL_ERR_INVALID_ARG, "stored_trans_mask must be in 0..3");
+  ccl::L2Config c;
+  c.l2_bytes = config->l2_bytes;
+  c.ways = config->ways;
+  c.line = config->line_bytes;
+  c.slots = config->slots;
+  c.k_step = config->k_step;
+  c.traversal = config->traversal;
+  c.threads = config->threads;
+  std::string why = ccl::check_l2_config(c);
+  if (why.empty() && c.line > plan->plan.page) why = "line_bytes must not exceed the page size";
+  if (!why.empty()) return fail(CCL_ERR_INVALID_ARG, why);
+  ccl::L2Traffic t;
+  try {
+    t = ccl::remote_bytes_l2(plan->plan, static_cast<ccl::Placement>(placement), stored_trans_mask, c);
+  } catch (const std::exception& e) {
+    return fail(CCL_ERR_INVALID_ARG, std::string("simulation failed: ") + e.what());
+  }
+  std::memset(out, 0, sizeof(*out));
+  for (int i = 0; i < 2; ++i) {
+    out->accesses[i] = t.accesses[i];
+    out->misses[i] = t.misses[i];
+  }
+  for (int i = 0; i < 3; ++i) out->remote[i] = t.remote[i];
   for (int i = 0; i < t.chiplets; ++i) out->remote_per_chiplet[i] = t.remote_per_chiplet[i];
   out->chiplets = t.chiplets;
   return ok();
