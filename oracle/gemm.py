@@ -34,6 +34,20 @@ def gemm_fp64(A: np.ndarray, B: np.ndarray) -> np.ndarray:
     return A @ B
 
 
+def gemm_scaled_fp64(A, B, C, alpha: float, beta: float) -> np.ndarray:
+    """alpha A B + beta C in float64 (the BLAS form of Sec. II-B).
+
+    As in BLAS, beta == 0 means C is not read at all (its values, NaN
+    included, do not matter).
+    """
+    P = gemm_fp64(A, B)
+    if beta == 0:
+        return alpha * P
+    if C.dtype == np.uint16:
+        C = decode_bf16(C)
+    return alpha * P + beta * C
+
+
 def gemm_entries(A: np.ndarray, B: np.ndarray, rows: np.ndarray, cols: np.ndarray) -> np.ndarray:
     """C[rows[i], cols[i]] for sampled output positions, in float64.
 

@@ -38,7 +38,8 @@ convention, identical in the library's implementation):
     misses * line.
   * C is written once per tile and is not allocated in L2 (the paper counts
     output writes to another chiplet separately from read misses); a C line
-    whose home is not the owner costs line bytes.
+    whose home is not the owner costs line bytes. With beta != 0 (c_read)
+    the tile's C lines are also read once, the same way, before the write.
 
 Pinned by (tests/test_oracle_l2sim.py): hand-worked LRU sequences; the
 LRU core against an independent reuse-distance computation; capacity 0
@@ -150,7 +151,8 @@ def partition_tiles(p, M, N, Gr, Gc, traversal):
 
 
 def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
-             l2_bytes, slots, ways=16, line=128, k_step=64, traversal="row", e=2):
+             l2_bytes, slots, ways=16, line=128, k_step=64, traversal="row", e=2,
+             c_read=False):
     """Remote-HBM traffic of C = A B with a private L2 per chiplet.
 
     Returns a dict of Python ints:
@@ -193,8 +195,9 @@ def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
                                             M, N, K, Gr, Gc, P, placement, 0, e, line)
                 for h in homes:
                     if h != p:
-                        rem["C"] += line
-                        per_chip[p] += line
+                        for _ in range(2 if c_read else 1):
+                            rem["C"] += line
+                            per_chip[p] += line
     return {
         "accesses": [acc["A"], acc["B"]],
         "misses": [mis["A"], mis["B"]],

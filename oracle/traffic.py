@@ -21,6 +21,10 @@ transposed (e.g. A = H^T held as H):
   CCL(P)     the operand is stored in CCL with strips padded to P, and every
              page of strip b is placed on chiplet b: chip = block b(r, c).
 
+With beta != 0 (C = alpha A B + beta C, Sec. II-B), the C tile is also read
+by its owner; the paper notes that this read is partitioned exactly like the
+write, so it is charged like the write (c_read=True doubles the C terms).
+
 Readings (the paper simulates per-chiplet L2 caches; this model has none, so
 it charges every tile's full panel reads; its ratios are not the paper's):
   see the notes at each function.
@@ -69,8 +73,8 @@ def _hist(chips: np.ndarray, G: int) -> np.ndarray:
     return np.bincount(chips.reshape(-1), minlength=G).astype(np.int64)
 
 
-def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2):
-    """Remote bytes of C = A B under one placement.
+def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2, c_read=False):
+    """Remote bytes of C = A B (or alpha A B + beta C with c_read) under one placement.
 
     Returns a dict of Python ints:
       accessed[A,B,C], remote[A,B,C], remote_per_chiplet[G],
@@ -103,7 +107,9 @@ def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2):
             rb = e * (K * TILE - int(h[o]))
             remote["B"] += rb
             per_chip[o] += rb
-    # C tiles: each written once by its owner (C is never stored transposed).
+    # C tiles: each written once by its owner (C is never stored transposed),
+    # and read once before that when c_read.
+    c_times = 2 if c_read else 1
     cols = np.arange(N)
     for ti in range(TM):
         rows = np.arange(ti * TILE, (ti + 1) * TILE)
@@ -111,11 +117,11 @@ def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2):
         ch = ch.reshape(TILE, TN, TILE).transpose(1, 0, 2).reshape(TN, -1)
         for tj in range(TN):
             o = own[ti, tj]
-            rb = e * int(np.count_nonzero(ch[tj] != o))
+            rb = c_times * e * int(np.count_nonzero(ch[tj] != o))
             remote["C"] += rb
             per_chip[o] += rb
 
-    accessed = {"A": e * M * K * TN, "B": e * K * N * TM, "C": e * M * N}
+    accessed = {"A": e * M * K * TN, "B": e * K * N * TM, "C": c_times * e * M * N}
     if placement == CCL:
         fp = {op: layout.total_bytes(*layout.operand_shape(op, M, N, K), Gr, Gc, P, e) for op in OPS}
     else:

@@ -61,3 +61,35 @@ def test_error_metrics_on_known_perturbation():
 def test_inner_dimension_mismatch_raises():
     with pytest.raises(ValueError):
         O.gemm_fp64(np.zeros((2, 3)), np.zeros((4, 2)))
+
+
+def test_scaled_gemm_on_integers_is_exact():
+    """alpha A B + beta C on ternary inputs, against exact integer arithmetic
+    (alpha, beta powers of two, so every value is exact in float64)."""
+    A = W.draw_array(71, 64, 96, "ternary")
+    B = W.draw_array(72, 96, 80, "ternary")
+    C = W.draw_array(73, 64, 80, "ternary")
+    ai = O.decode_bf16(A).astype(np.int64)
+    bi = O.decode_bf16(B).astype(np.int64)
+    ci = O.decode_bf16(C).astype(np.int64)
+    for alpha, beta in ((1.0, 0.0), (0.5, 2.0), (-2.0, -1.0), (0.0, 4.0)):
+        exact = alpha * (ai @ bi).astype(np.float64) + beta * ci.astype(np.float64)
+        assert np.array_equal(O.gemm_scaled_fp64(A, B, C, alpha, beta), exact)
+
+
+def test_scaled_gemm_beta_zero_ignores_c():
+    A = W.draw_array(74, 32, 48)
+    B = W.draw_array(75, 48, 16)
+    C = np.full((32, 16), 0x7FC0, dtype=np.uint16)          # bf16 NaN everywhere
+    out = O.gemm_scaled_fp64(A, B, C, 1.5, 0.0)
+    assert np.all(np.isfinite(out))
+    assert np.array_equal(out, 1.5 * O.gemm_fp64(A, B))
+
+
+def test_scaled_gemm_identity_a():
+    """A = I: alpha B + beta C elementwise."""
+    B = W.draw_array(76, 64, 32)
+    C = W.draw_array(77, 64, 32)
+    eye = np.eye(64)
+    got = O.gemm_scaled_fp64(eye, B, C, 0.25, -3.0)
+    assert np.array_equal(got, 0.25 * O.decode_bf16(B) - 3.0 * O.decode_bf16(C))

@@ -237,3 +237,16 @@ def test_order_traversal():
     assert row["misses"] == [256, 512]
     assert col["misses"] == [512, 256]
 
+
+
+@pytest.mark.parametrize("placement", PLACEMENTS)
+def test_c_read_is_charged_like_the_write(placement):
+    M, N, K, Gr, Gc, P = 256, 512, 256, 2, 2, 4096
+    ref = T.remote_bytes(M, N, K, Gr, Gc, P, placement, c_read=True)
+    got = L.simulate(M, N, K, Gr, Gc, P, placement, l2_bytes=0, slots=2, c_read=True)
+    assert got["remote"] == ref["remote"]
+    plain = L.simulate(M, N, K, Gr, Gc, P, placement, l2_bytes=4 * 16 * 128, slots=2)
+    read = L.simulate(M, N, K, Gr, Gc, P, placement, l2_bytes=4 * 16 * 128, slots=2, c_read=True)
+    assert read["remote"][:2] == plain["remote"][:2]
+    assert read["remote"][2] == 2 * plain["remote"][2]
+    assert read["misses"] == plain["misses"]

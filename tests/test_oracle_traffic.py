@@ -58,7 +58,7 @@ def _chip_matrix(R, Cc, trans, placement, Gr, Gc, P, e=2):
     return _page_table(n_pages, G, placement)[addr // P]
 
 
-def brute_remote(M, N, K, Gr, Gc, P, placement, ta=0, tb=0, chips=None, e=2):
+def brute_remote(M, N, K, Gr, Gc, P, placement, ta=0, tb=0, chips=None, e=2, c_read=False):
     G = Gr * Gc
     if chips is None:
         chips = (_chip_matrix(M, K, ta, placement, Gr, Gc, P),
@@ -72,8 +72,11 @@ def brute_remote(M, N, K, Gr, Gc, P, placement, ta=0, tb=0, chips=None, e=2):
     for m0 in range(0, M, 128):
         for n0 in range(0, N, 128):
             own = (m0 // rows_per_part) * Gc + (n0 // cols_per_part)
-            for i, blk in enumerate((chA[m0:m0 + 128, :], chB[:, n0:n0 + 128],
-                                     chC[m0:m0 + 128, n0:n0 + 128])):
+            blocks = [(0, chA[m0:m0 + 128, :]), (1, chB[:, n0:n0 + 128]),
+                      (2, chC[m0:m0 + 128, n0:n0 + 128])]
+            if c_read:                          # beta != 0: the C tile is read too
+                blocks.append((2, chC[m0:m0 + 128, n0:n0 + 128]))
+            for i, blk in blocks:
                 nb = e * int(np.count_nonzero(blk != own))
                 remote[i] += nb
                 accessed[i] += e * blk.size
@@ -104,6 +107,17 @@ def test_histogram_model_equals_brute_force(M, N, K, Gr, Gc, P, ta, tb, placemen
     assert rec["remote"] == remote
     assert rec["accessed"] == accessed
     assert rec["remote_per_chiplet"] == per
+
+
+@pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", CASES[:5])
+@pytest.mark.parametrize("placement", T.PLACEMENTS)
+def test_c_read_equals_brute_force(M, N, K, Gr, Gc, P, ta, tb, placement):
+    rec = T.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb, c_read=True)
+    remote, accessed, per = brute_remote(M, N, K, Gr, Gc, P, placement, ta, tb, c_read=True)
+    assert rec["remote"] == remote
+    assert rec["accessed"] == accessed
+    assert rec["remote_per_chiplet"] == per
+    assert rec["accessed"][2] == 2 * 2 * M * N
 
 
 @pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", CASES)

@@ -11,6 +11,10 @@ Workloads (LLM FFN GEMMs, Sec. IV-A "Workloads"; bf16 operands):
   llama_fwd   X[8192x8192] W_up[8192x28672]; H[8192x28672] W_down[28672x8192]
   llama_bwd   dW_up = X^T dY and dX = dY W_up^T (dY 8192x28672)
 
+The sweep of Sec. IV-A: the FFN gate/up and down projections of both models,
+in the forward pass and both backward GEMMs (dX, dW), at 4K, 8K and 16K
+tokens: 36 GEMM shapes (FFN_SWEEP; shapes only, no data).
+
 Seeds: 1000 * workload number + index of the tensor in its workload, in
 order of first appearance. Normal distributions are parameterised by their
 standard deviation.
@@ -113,6 +117,46 @@ def _workloads():
 
 
 WORKLOADS = _workloads()
+
+
+@dataclass(frozen=True)
+class SweepGemm:
+    """One GEMM of the FFN sweep: C = A B with A (M x K), B (K x N)."""
+    model: str
+    tokens: int
+    proj: str            # "gate_up" or "down"
+    pass_: str           # "fwd" (Y = X W), "dX" (dY W^T), "dW" (X^T dY)
+    M: int
+    N: int
+    K: int
+    a_trans: int         # A stored transposed (X^T held as X)
+    b_trans: int         # B stored transposed (W^T held as W)
+
+    @property
+    def name(self) -> str:
+        return f"{self.model}/{self.proj}/{self.pass_}/{self.tokens // 1024}K"
+
+
+# hidden size, gate/up output width, down input width
+FFN_MODELS = {
+    "qwen3_30b": (2048, 1536, 768),        # one expert MLP, gate and up fused (2 x 768)
+    "llama31_70b": (8192, 28672, 28672),   # the up (or gate) projection, as in llama_fwd
+}
+SWEEP_TOKENS = (4096, 8192, 16384)
+
+
+def _ffn_sweep():
+    out = []
+    for model, (d, fg, f) in FFN_MODELS.items():
+        for T in SWEEP_TOKENS:
+            for proj, din, dout in (("gate_up", d, fg), ("down", f, d)):
+                out.append(SweepGemm(model, T, proj, "fwd", T, dout, din, 0, 0))
+                out.append(SweepGemm(model, T, proj, "dX", T, din, dout, 0, 1))
+                out.append(SweepGemm(model, T, proj, "dW", din, dout, T, 1, 0))
+    return tuple(out)
+
+
+FFN_SWEEP = _ffn_sweep()
 
 
 def gemm_by_name(name: str) -> tuple[Workload, Gemm]:
