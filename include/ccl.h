@@ -149,6 +149,18 @@ ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void*
                     void* stream);
 
 /*
+ * C_ccl = alpha * A_ccl B_ccl + beta * C_ccl, the BLAS form of the GEMM
+ * (Sec. II-B): the scalars change no placement, and each output tile's owner
+ * reads its C tile where it writes it. The product is accumulated in fp32,
+ * then alpha * acc + beta * c is formed in fp32 and rounded to bf16 (nearest
+ * even). beta == 0: C is not read (its old contents, NaN included, do not
+ * matter), as in BLAS. ccl_gemm is alpha = 1, beta = 0.
+ * Errors as ccl_gemm.
+ */
+ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, const void* B_ccl,
+                           float beta, void* C_ccl, void* stream);
+
+/*
  * Baseline for comparison with ccl_gemm (the layout the paper starts from,
  * Sec. II-B Eq. 2): the same GEMM kernel on plain row-major operands
  * A (M x K), B (K x N) and C (M x N), leading dimensions K, N and N, with
@@ -161,13 +173,21 @@ ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void*
 ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void* C, int remap,
                              void* stream);
 
+/* Flags of ccl_remote_bytes and ccl_remote_bytes_l2. */
+#define CCL_TRAFFIC_A_TRANS 1   /* A is stored transposed (e.g. H held for A = H^T) */
+#define CCL_TRAFFIC_B_TRANS 2   /* B is stored transposed */
+#define CCL_TRAFFIC_C_READ 4    /* C is read as well as written: alpha A B + beta C,
+                                   beta != 0 (Sec. II-B: the read is partitioned
+                                   like the write, so each tile's owner reads it) */
+
 /*
  * Remote-byte record of the plan's GEMM under `placement` (Sec. IV-A).
- * stored_trans_mask bit 0: A is stored transposed; bit 1: B is stored
- * transposed (affects RR and COARSE only: they place pages of the stored
- * tensor). Host-only, synchronous. Errors: CCL_ERR_INVALID_ARG.
+ * flags: CCL_TRAFFIC_* bits. The stored-transpose bits affect RR and COARSE
+ * only (they place pages of the stored tensor); CCL_TRAFFIC_C_READ charges
+ * each C tile a read as well as the write. Host-only, synchronous.
+ * Errors: CCL_ERR_INVALID_ARG (NULL argument, bad placement, flags outside 0..7).
  */
-ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int flags,
                             ccl_traffic* out);
 
 /* Private L2 of each chiplet for ccl_remote_bytes_l2 (Sec. IV-A: the
@@ -202,18 +222,19 @@ typedef struct {
  *     k_step at a time, and at each step each tile (in wave order) reads the
  *     lines of its A slice (128 x k_step) and then of its B slice
  *     (k_step x 128), each in increasing address order of the operand as
- *     stored (row-major, stored transposed per stored_trans_mask, or CCL);
+ *     stored (row-major, stored transposed per the flags, or CCL);
  *   - A is at address 0, B at 2^40, C at 2^41; a line's set is its line
  *     number XOR-folded into log2(sets) bits; replacement is LRU;
  *   - a miss is remote when the line's home chiplet under `placement` (as in
  *     ccl_remote_bytes) is not p; after a wave, its C tiles are written
- *     without allocating in L2, and every C line homed elsewhere counts.
+ *     (and first read, with CCL_TRAFFIC_C_READ) without allocating in L2,
+ *     and every C line homed elsewhere counts each time.
  * With l2_bytes = 0 and line-aligned slices the result equals
  * ccl_remote_bytes. Host-only, synchronous; runs one host thread per chiplet.
- * Errors: CCL_ERR_INVALID_ARG (NULL argument, bad placement or mask,
- * invalid configuration).
+ * Errors: CCL_ERR_INVALID_ARG (NULL argument, bad placement, flags outside
+ * 0..7, invalid configuration).
  */
-ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int flags,
                                const ccl_l2_config* config, ccl_l2_traffic* out);
 
 /* Static name of a status code. */

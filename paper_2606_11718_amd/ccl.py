@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 
 # every symbol include/ccl.h declares
 EXPORTED = ("ccl_plan", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
-            "ccl_unpack", "ccl_gemm", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
+            "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
@@ -85,6 +85,7 @@ def library() -> ctypes.CDLL:
         "ccl_pack": [vp, i32, vp, i64, i32, vp, vp],
         "ccl_unpack": [vp, i32, vp, vp, i64, vp],
         "ccl_gemm": [vp, vp, vp, vp, vp],
+        "ccl_gemm_scaled": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, vp],
         "ccl_gemm_rowmajor": [vp, vp, vp, vp, i32, vp],
         "ccl_remote_bytes": [vp, i32, i32, ctypes.POINTER(_Traffic)],
         "ccl_remote_bytes_l2": [vp, i32, i32, ctypes.POINTER(_L2Config), ctypes.POINTER(_L2Traffic)],
@@ -189,13 +190,21 @@ def ccl_gemm(plan: Plan, A_ccl, B_ccl, C_ccl, stream=None) -> None:
     _check(library().ccl_gemm(plan, _ptr(A_ccl), _ptr(B_ccl), _ptr(C_ccl), _stream(stream)))
 
 
+def ccl_gemm_scaled(plan: Plan, alpha: float, A_ccl, B_ccl, beta: float, C_ccl, stream=None) -> None:
+    _check(library().ccl_gemm_scaled(plan, alpha, _ptr(A_ccl), _ptr(B_ccl), beta, _ptr(C_ccl),
+                                     _stream(stream)))
+
+
 def ccl_gemm_rowmajor(plan: Plan, A, B, C, remap: int, stream=None) -> None:
     _check(library().ccl_gemm_rowmajor(plan, _ptr(A), _ptr(B), _ptr(C), remap, _stream(stream)))
 
 
-def ccl_remote_bytes(plan: Plan, placement: int, stored_trans_mask: int) -> dict:
+CCL_TRAFFIC_A_TRANS, CCL_TRAFFIC_B_TRANS, CCL_TRAFFIC_C_READ = 1, 2, 4
+
+
+def ccl_remote_bytes(plan: Plan, placement: int, flags: int) -> dict:
     t = _Traffic()
-    _check(library().ccl_remote_bytes(plan, placement, stored_trans_mask, ctypes.byref(t)))
+    _check(library().ccl_remote_bytes(plan, placement, flags, ctypes.byref(t)))
     return {
         "accessed": list(t.accessed),
         "remote": list(t.remote),
@@ -205,12 +214,12 @@ def ccl_remote_bytes(plan: Plan, placement: int, stored_trans_mask: int) -> dict
     }
 
 
-def ccl_remote_bytes_l2(plan: Plan, placement: int, stored_trans_mask: int, *, l2_bytes: int,
+def ccl_remote_bytes_l2(plan: Plan, placement: int, flags: int, *, l2_bytes: int,
                         slots: int, ways: int = 16, line_bytes: int = 128, k_step: int = 64,
                         traversal: int = 0, threads: int = 0) -> dict:
     cfg = _L2Config(l2_bytes, ways, line_bytes, slots, k_step, traversal, threads)
     t = _L2Traffic()
-    _check(library().ccl_remote_bytes_l2(plan, placement, stored_trans_mask, ctypes.byref(cfg),
+    _check(library().ccl_remote_bytes_l2(plan, placement, flags, ctypes.byref(cfg),
                                          ctypes.byref(t)))
     return {
         "accesses": list(t.accesses),

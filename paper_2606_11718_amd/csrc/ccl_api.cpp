@@ -169,8 +169,8 @@ ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void
                     "unpack launch");
 }
 
-ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
-                    void* stream) {
+ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, const void* B_ccl,
+                           float beta, void* C_ccl, void* stream) {
   if (!plan || !A_ccl || !B_ccl || !C_ccl) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
   if (!aligned16(A_ccl) || !aligned16(B_ccl) || !aligned16(C_ccl))
     return fail(CCL_ERR_MISALIGNED_POINTER, "A, B and C must be 16-byte aligned");
@@ -180,9 +180,14 @@ ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void*
   ccl_addressing(p, &a, &b, &c);
   if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
   if (ccl_status s = check_device()) return s;
-  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true,
+  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, alpha, beta,
                                      static_cast<hipStream_t>(stream)),
                     "gemm launch");
+}
+
+ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
+                    void* stream) {
+  return ccl_gemm_scaled(plan, 1.f, A_ccl, B_ccl, 0.f, C_ccl, stream);
 }
 
 ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void* C, int remap,
@@ -197,19 +202,18 @@ ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void
   rowmajor_addressing(p, &a, &b, &c);
   if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "rows too long for 32-bit in-tile offsets");
   if (ccl_status s = check_device()) return s;
-  return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1,
+  return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1, 1.f, 0.f,
                                      static_cast<hipStream_t>(stream)),
                     "gemm launch");
 }
 
-ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int flags,
                             ccl_traffic* out) {
   if (!plan || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
   if (placement != CCL_PLACE_RR && placement != CCL_PLACE_COARSE && placement != CCL_PLACE_CCL)
     return fail(CCL_ERR_INVALID_ARG, "unknown placement");
-  if (stored_trans_mask < 0 || stored_trans_mask > 3)
-    return fail(CCL_ERR_INVALID_ARG, "stored_trans_mask must be in 0..3");
-  ccl::Traffic t = ccl::remote_bytes(plan->plan, static_cast<ccl::Placement>(placement), stored_trans_mask);
+  if (flags < 0 || flags > 7) return fail(CCL_ERR_INVALID_ARG, "flags must be in 0..7");
+  ccl::Traffic t = ccl::remote_bytes(plan->plan, static_cast<ccl::Placement>(placement), flags);
   std::memset(out, 0, sizeof(*out));
   for (int i = 0; i < 3; ++i) {
     out->accessed[i] = t.accessed[i];
@@ -222,13 +226,12 @@ ccl_status ccl_remote_bytes(ccl_plan_t plan, ccl_placement placement, int stored
   return ok();
 }
 
-ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int stored_trans_mask,
+ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int flags,
                                const ccl_l2_config* config, ccl_l2_traffic* out) {
   if (!plan || !config || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
   if (placement != CCL_PLACE_RR && placement != CCL_PLACE_COARSE && placement != CCL_PLACE_CCL)
     return fail(CCL_ERR_INVALID_ARG, "unknown placement");
-  if (stored_trans_mask < 0 || stored_trans_mask > 3)
-    return fail(CCL_ERR_INVALID_ARG, "stored_trans_mask must be in 0..3");
+  if (flags < 0 || flags > 7) return fail(CCL_ERR_INVALID_ARG, "flags must be in 0..7");
   ccl::L2Config c;
   c.l2_bytes = config->l2_bytes;
   c.ways = config->ways;
@@ -242,7 +245,7 @@ ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int sto
   if (!why.empty()) return fail(CCL_ERR_INVALID_ARG, why);
   ccl::L2Traffic t;
   try {
-    t = ccl::remote_bytes_l2(plan->plan, static_cast<ccl::Placement>(placement), stored_trans_mask, c);
+    t = ccl::remote_bytes_l2(plan->plan, static_cast<ccl::Placement>(placement), flags, c);
   } catch (const std::exception& e) {
     return fail(CCL_ERR_INVALID_ARG, std::string("simulation failed: ") + e.what());
   }

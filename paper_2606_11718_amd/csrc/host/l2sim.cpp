@@ -10,7 +10,7 @@
 // a set. A miss is remote when the line's home chiplet under the placement is
 // not the one running the tile. When a wave has finished K, each of its tiles
 // writes its C tile, which is not cached; each C line homed elsewhere costs
-// one line of remote traffic.
+// one line of remote traffic (two when C is also read, beta != 0).
 //
 // Chiplets have private caches and are simulated independently, one host
 // thread each.
@@ -161,7 +161,8 @@ struct ChipletCount {
   uint64_t accesses[2] = {0, 0}, misses[2] = {0, 0}, remote[3] = {0, 0, 0};
 };
 
-ChipletCount simulate_chiplet(const Plan& p, int chip, const Stored* st, const L2Config& c) {
+ChipletCount simulate_chiplet(const Plan& p, int chip, const Stored* st, const L2Config& c,
+                              uint64_t c_times) {
   ChipletCount out;
   Lru cache(c.l2_bytes, c.ways, c.line);
   int shift = 0;
@@ -207,7 +208,7 @@ ChipletCount simulate_chiplet(const Plan& p, int chip, const Stored* st, const L
       int64_t ti, tj;
       tile(w0 + j, &ti, &tj);
       for_each_line(st[OP_C], ti * T, ti * T + T, tj * T, tj * T + T, shift, [&](int64_t off) {
-        if (st[OP_C].home(off) != chip) out.remote[2] += uint64_t(c.line);
+        if (st[OP_C].home(off) != chip) out.remote[2] += c_times * uint64_t(c.line);
       });
     }
   }
@@ -235,7 +236,9 @@ std::string check_l2_config(const L2Config& c) {
   return "";
 }
 
-L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int trans_mask, const L2Config& c) {
+L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int flags, const L2Config& c) {
+  const int trans_mask = flags & 3;
+  const uint64_t c_times = (flags & kTrafficCRead) ? 2 : 1;
   Stored st[3] = {make_stored(p, OP_A, pl, trans_mask & 1, c.line),
                   make_stored(p, OP_B, pl, (trans_mask >> 1) & 1, c.line),
                   make_stored(p, OP_C, pl, false, c.line)};
@@ -245,7 +248,7 @@ L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int trans_mask, const L2C
   nthreads = std::min(nthreads, p.G);
   std::atomic<int> next{0};
   auto worker = [&] {
-    for (int chip; (chip = next.fetch_add(1)) < p.G;) per[chip] = simulate_chiplet(p, chip, st, c);
+    for (int chip; (chip = next.fetch_add(1)) < p.G;) per[chip] = simulate_chiplet(p, chip, st, c, c_times);
   };
   if (nthreads <= 1) {
     worker();

@@ -30,6 +30,7 @@ struct L2Traffic {
 // Validate a configuration; empty string when usable.
 std::string check_l2_config(const L2Config& c);
 
-L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int trans_mask, const L2Config& c);
+// flags as for remote_bytes (plan.hpp).
+L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int flags, const L2Config& c);
 
 }  // namespace ccl

@@ -241,7 +241,9 @@ Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, i
   return Status::OK;
 }
 
-Traffic remote_bytes(const Plan& p, Placement pl, int trans_mask) {
+Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
+  const int trans_mask = flags & 3;
+  const uint64_t c_times = (flags & kTrafficCRead) ? 2 : 1;   // beta != 0: C read, then written
   Traffic t;
   t.chiplets = p.G;
   const int G = p.G;
@@ -284,20 +286,21 @@ Traffic remote_bytes(const Plan& p, Placement pl, int trans_mask) {
       t.remote_per_chiplet[o] += rem;
     }
   }
-  // C: each tile written once by its owner.
+  // C: each tile written once by its owner (and read once before that when
+  // c_times == 2; the read has the write's partitioning).
   for (int64_t ti = 0; ti < TM; ++ti) {
     for (int64_t tj = 0; tj < TN; ++tj) {
       std::fill(h.begin(), h.end(), 0);
       ops[OP_C].count(ti * T, (ti + 1) * T, tj * T, (tj + 1) * T, h.data());
       const int o = p.owner(ti, tj);
-      uint64_t rem = e * ((uint64_t)(T * T) - h[o]);
+      uint64_t rem = c_times * e * ((uint64_t)(T * T) - h[o]);
       t.remote[OP_C] += rem;
       t.remote_per_chiplet[o] += rem;
     }
   }
   t.accessed[OP_A] = e * (uint64_t)p.M * p.K * TN;
   t.accessed[OP_B] = e * (uint64_t)p.K * p.N * TM;
-  t.accessed[OP_C] = e * (uint64_t)p.M * p.N;
+  t.accessed[OP_C] = c_times * e * (uint64_t)p.M * p.N;
   t.floor_bytes = floor_bytes(p.M, p.N, p.K, p.Gr, p.Gc);
   return t;
 }

@@ -82,9 +82,12 @@ bool grid_aligned(int64_t M, int64_t N, int64_t K, int G, int Gr);
 // Remote bytes of CCL (the floor): e*M*N*K*[(Gc-1)/(Gc*128) + (Gr-1)/(Gr*128)].
 uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc);
 
-// The remote-byte model under one placement. Stored-transpose flags apply
-// to A and B (bit 0, bit 1).
-Traffic remote_bytes(const Plan& p, Placement pl, int trans_mask);
+// Traffic flags: bit 0 A stored transposed, bit 1 B stored transposed,
+// bit 2 C is read as well as written (alpha A B + beta C with beta != 0).
+constexpr int kTrafficCRead = 4;
+
+// The remote-byte model under one placement.
+Traffic remote_bytes(const Plan& p, Placement pl, int flags);
 
 // Parameters of the workgroup -> tile map of the GEMM launch.
 TileMap tile_map(const Plan& p);

@@ -1,18 +1,19 @@
-// C = A B on CCL operands for gfx950 (Sec. II-B, III-C: the arithmetic is
-// the plain tiled GEMM; only the operand address map is CCL's).
+// C = A B (or alpha A B + beta C) on CCL operands for gfx950 (Sec. II-B,
+// III-C: the arithmetic is the plain tiled GEMM; only the operand address
+// map is CCL's).
 //
-// Workgroup = 4 waves (2 x 2), output tile BM x BN, K step 64.
+// Workgroup = 2 x WGN waves, output tile BM x BN, K step 32 (kBK).
 //  * Workgroup -> tile: tile_map.hpp. Dispatch is round-robin over the 8
 //    XCDs, so the map sends every tile to an XCD of the chiplet that owns
 //    it (Sec. III-A).
 //  * Operand addressing: inside one CCL block an operand is row-major with
 //    leading dimension wc; A changes block every K/Gc columns and B every
-//    K/Gr rows, which a K step (64) never straddles. The same descriptor
-//    also expresses plain row-major operands.
-//  * Global -> LDS: direct-to-LDS 16-byte loads (global_load_lds_dwordx4),
-//    two LDS stages; the next K step is in flight while MFMAs run on the
-//    current one. Which 16-byte chunk each lane fetches is permuted (XOR
-//    swizzle) so the fragment reads below hit distinct LDS banks.
+//    K/Gr rows, which a K step never straddles. The same descriptor also
+//    expresses plain row-major operands.
+//  * Global -> LDS: direct-to-LDS 16-byte buffer loads, four LDS stages; the
+//    loads of step s+3 are issued while the MFMAs of step s run. Which
+//    16-byte chunk each lane fetches is permuted (XOR swizzle) so the
+//    fragment reads below hit distinct LDS banks.
 //  * A (K contiguous) fragments: ds_read_b128. B (N contiguous) fragments:
 //    ds_read_b64_tr_b16, which transposes 16-bit data across each group of
 //    16 lanes (lane l, element j <- lane 4j + l/4, element l%4).
@@ -48,6 +49,8 @@ struct GemmParams {
   int32_t ksteps;       // K / 32
   int32_t remap;        // 1: XCD-aware map; 0: native raster over the whole C
   int32_t grid_r;       // Gr (native raster)
+  int32_t epi;          // epilogue: 0 acc, 1 alpha*acc, 2 alpha*acc + beta*C (C read)
+  float alpha, beta;
 };
 
 // LDS chunk swizzles (16-byte chunk index XOR a function of the row).
@@ -342,6 +345,8 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 
   // ---- epilogue: lane holds C[m][n .. n+3] for each (mt, nt, q) ----
   uint16_t* c_tile = p.C + pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  const int epi = p.epi;
+  const float alpha = p.alpha, beta = p.beta;
 #pragma unroll
   for (int mt = 0; mt < T::TM; ++mt) {
     const int m = wm * T::WM + mt * 32 + (lane & 31);
@@ -350,10 +355,22 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = wn * T::WN + nt * 32 + 8 * q + 4 * (lane >> 5);
+        uint2* dst = reinterpret_cast<uint2*>(c_tile + (int64_t)m * p.c.ld + n);
+        float o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
+        if (epi != 0) {
+          uint2 old = make_uint2(0u, 0u);
+          if (epi == 2) old = *dst;
+          const float c[4] = {__uint_as_float(old.x << 16), __uint_as_float(old.x & 0xffff0000u),
+                              __uint_as_float(old.y << 16), __uint_as_float(old.y & 0xffff0000u)};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * c[j]) : alpha * o[j];
+        }
         uint2 v;
-        v.x = bf16_rne(acc[mt][nt][4 * q + 0]) | (bf16_rne(acc[mt][nt][4 * q + 1]) << 16);
-        v.y = bf16_rne(acc[mt][nt][4 * q + 2]) | (bf16_rne(acc[mt][nt][4 * q + 3]) << 16);
-        *reinterpret_cast<uint2*>(c_tile + (int64_t)m * p.c.ld + n) = v;
+        v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
+        v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
+        *dst = v;
       }
     }
   }
@@ -382,7 +399,7 @@ __global__ void __launch_bounds__(64) dispatch_probe_kernel(TileMap map, int32_t
 
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
-                       bool remap, hipStream_t stream) {
+                       bool remap, float alpha, float beta, hipStream_t stream) {
   const GemmConfig& g = p.gemm;
   GemmParams gp;
   gp.A = static_cast<const uint16_t*>(A);
@@ -395,6 +412,9 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   gp.ksteps = (int32_t)(p.K / kBK);
   gp.remap = remap ? 1 : 0;
   gp.grid_r = p.Gr;
+  gp.alpha = alpha;
+  gp.beta = beta;
+  gp.epi = beta != 0.f ? 2 : (alpha != 1.f ? 1 : 0);
   const unsigned wgs = remap ? (unsigned)g.workgroups
                              : (unsigned)(g.tiles_m * g.tiles_n * p.G);
   dim3 grid(wgs);

@@ -26,10 +26,11 @@ hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, 
 // Pack from a stored transpose (cols x rows, leading dimension ld).
 hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld, void* dst,
                              hipStream_t stream);
-// C = A B with the given operand addressing; remap = XCD-aware tile map.
+// C = alpha A B + beta C with the given operand addressing; remap =
+// XCD-aware tile map. C is read only when beta != 0.
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
-                       bool remap, hipStream_t stream);
+                       bool remap, float alpha, float beta, hipStream_t stream);
 // Dispatch probe with the GEMM grid (4 int32 per workgroup).
 hipError_t launch_dispatch_probe(const Plan& p, int32_t* out, hipStream_t stream);
 

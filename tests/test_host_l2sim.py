@@ -24,15 +24,16 @@ PLACE = {"rr": ccl.CCL_PLACE_RR, "coarse": ccl.CCL_PLACE_COARSE, "ccl": ccl.CCL_
 TRAV = {"row": 0, "col": 1}
 
 
-def _both(M, N, K, G, Gr, P, placement, ta, tb, **cfg):
+def _both(M, N, K, G, Gr, P, placement, ta, tb, c_read=False, **cfg):
     plan = ccl.ccl_plan(M, N, K, G, Gr, P)
-    lib = ccl.ccl_remote_bytes_l2(plan, PLACE[placement], ta | (tb << 1),
+    flags = ta | (tb << 1) | (ccl.CCL_TRAFFIC_C_READ if c_read else 0)
+    lib = ccl.ccl_remote_bytes_l2(plan, PLACE[placement], flags,
                                   l2_bytes=cfg["l2_bytes"], slots=cfg["slots"], ways=cfg["ways"],
                                   line_bytes=cfg.get("line", 128), k_step=cfg["k_step"],
                                   traversal=TRAV[cfg["traversal"]])
     ora = L.simulate(M, N, K, Gr, G // Gr, P, placement, ta, tb, l2_bytes=cfg["l2_bytes"],
                      slots=cfg["slots"], ways=cfg["ways"], line=cfg.get("line", 128),
-                     k_step=cfg["k_step"], traversal=cfg["traversal"])
+                     k_step=cfg["k_step"], traversal=cfg["traversal"], c_read=c_read)
     return lib, ora
 
 
@@ -62,6 +63,13 @@ def test_small_shapes_match_oracle(shape, placement):
         for cfg in CFGS:
             lib, ora = _both(M, N, K, G, Gr, P, placement, mask & 1, mask >> 1, **cfg)
             assert lib == ora, (shape, placement, mask, cfg)
+
+
+@pytest.mark.parametrize("placement", ["rr", "coarse", "ccl"])
+def test_c_read_matches_oracle(placement):
+    for cfg in CFGS[:3]:
+        lib, ora = _both(256, 512, 256, 4, 2, 4096, placement, 0, 1, c_read=True, **cfg)
+        assert lib == ora
 
 
 def test_line_sizes_match_oracle():
@@ -135,7 +143,7 @@ def test_rejects_bad_config(bad):
 
 def test_rejects_bad_placement_and_mask():
     plan = ccl.ccl_plan(256, 512, 256, 4, 2, 4096)
-    for pl, mask in ((3, 0), (-1, 0), (0, 4), (0, -1)):
+    for pl, mask in ((3, 0), (-1, 0), (0, 8), (0, -1)):
         with pytest.raises(ccl.CCLError) as ei:
             ccl.ccl_remote_bytes_l2(plan, pl, mask, l2_bytes=0, slots=1)
         assert ei.value.status == 1

@@ -72,7 +72,8 @@ def test_null_arguments_are_rejected_without_gpu():
     assert lib.ccl_plan_layout(p, 0, None) == 1
     assert lib.ccl_plan_layout(p, 7, ctypes.byref(ccl._Layout())) == 1
     assert lib.ccl_remote_bytes(p, 5, 0, ctypes.byref(ccl._Traffic())) == 1
-    assert lib.ccl_remote_bytes(p, 0, 4, ctypes.byref(ccl._Traffic())) == 1
+    assert lib.ccl_remote_bytes(p, 0, 8, ctypes.byref(ccl._Traffic())) == 1
+    assert lib.ccl_remote_bytes(p, 0, -1, ctypes.byref(ccl._Traffic())) == 1
     assert lib.ccl_gemm(p, None, None, None, None) == 1
     assert lib.ccl_gemm(p, 16, 32, 8, None) == 4            # misaligned pointer
     assert lib.ccl_pack(p, 0, None, 256, 0, None, None) == 1
@@ -144,10 +145,12 @@ RANDOM_SHAPES = [
 @pytest.mark.parametrize("placement", OT.PLACEMENTS)
 def test_remote_bytes_match_oracle_small(M, N, K, Gr, Gc, P, ta, tb, placement):
     p = ccl.ccl_plan(M, N, K, Gr * Gc, Gr, P)
-    got = ccl.ccl_remote_bytes(p, PLACE[placement], ta | (tb << 1))
-    ref = OT.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb)
-    for k in ("accessed", "remote", "remote_per_chiplet", "floor", "footprint"):
-        assert got[k] == ref[k], k
+    for c_read in (False, True):
+        flags = ta | (tb << 1) | (ccl.CCL_TRAFFIC_C_READ if c_read else 0)
+        got = ccl.ccl_remote_bytes(p, PLACE[placement], flags)
+        ref = OT.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb, c_read=c_read)
+        for k in ("accessed", "remote", "remote_per_chiplet", "floor", "footprint"):
+            assert got[k] == ref[k], (k, c_read)
 
 
 TILE_CASES = [(256, 512, 256, 4, 2), (4096, 1536, 2048, 8, 2), (768, 2048, 4096, 8, 1),
@@ -186,3 +189,14 @@ def test_gemm_config_tiles_nest_in_partitions():
         tm_, tn_, _ = ccl.ccl_debug_gemm_config(p)
         assert (M // Gr) % tm_ == 0 and (N // (G // Gr)) % tn_ == 0
         assert tm_ in (128, 256) and tn_ in (128, 256)
+
+
+@pytest.mark.parametrize("T,D,F,G,Gr", [(8192, 8192, 28672, 8, 2), (4096, 2048, 1536, 8, 2),
+                                        (2048, 1024, 3072, 8, 4), (256, 256, 512, 4, 2)])
+def test_ffn_intermediate_needs_no_repack(T, D, F, G, Gr):
+    """C of X[T x D] W1[D x F] and A of H[T x F] W2[F x D] on the same grid are
+    the same CCL layout, so the first GEMM's output buffer is the second
+    GEMM's A buffer as it stands (activations produced directly in CCL)."""
+    up = ccl.ccl_plan(T, F, D, G, Gr, 4096)
+    down = ccl.ccl_plan(T, D, F, G, Gr, 4096)
+    assert ccl.ccl_plan_layout(up, ccl.CCL_C) == ccl.ccl_plan_layout(down, ccl.CCL_A)
