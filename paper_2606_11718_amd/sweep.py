@@ -66,10 +66,15 @@ def _remote(g, chiplets: int, grid_rows: int, placement: int, page: int, model: 
     return sum(rec["remote"])
 
 
-def evaluate(gemms, setting_name: str = "mi300x_like", model: str = "l2", workers: int = 0,
+def evaluate(gemms, setting_name="mi300x_like", model: str = "l2", workers: int = 0,
              log=None) -> list[dict]:
-    """Best (grid, traversal) remote bytes of every GEMM under every placement."""
-    setting = SETTINGS[setting_name]
+    """Best (grid, traversal) remote bytes of every GEMM under every placement.
+
+    setting_name: a key of SETTINGS, or a dict with the same fields.
+    """
+    setting = SETTINGS[setting_name] if isinstance(setting_name, str) else dict(setting_name)
+    if not isinstance(setting_name, str):
+        setting_name = "custom"
     G = setting["chiplets"]
     grids = [gr for gr in range(1, G + 1) if G % gr == 0]
     travs = (0, 1) if model == "l2" else (0,)
@@ -101,6 +106,10 @@ def evaluate(gemms, setting_name: str = "mi300x_like", model: str = "l2", worker
         rec = {"gemm": g.name, "model": g.model, "tokens": g.tokens, "proj": g.proj, "pass": g.pass_,
                "M": g.M, "N": g.N, "K": g.K, "trans_a": g.a_trans, "trans_b": g.b_trans,
                "setting": setting_name, "traffic_model": model}
+        if (gi, "ccl") not in best:        # no tile-aligned grid for this GEMM
+            rec["no_aligned_grid"] = True
+            out.append(rec)
+            continue
         for name, _, _ in PLACEMENTS:
             rb, gr, tr = best[(gi, name)]
             rec[name] = {"remote_bytes": rb, "grid": f"{gr}x{G // gr}",
@@ -118,7 +127,7 @@ def summarize(records: list[dict]) -> dict:
     """Per model: geometric means of placement / CCL and the fine-optimal count."""
     out = {}
     for model in sorted({r["model"] for r in records}):
-        rs = [r for r in records if r["model"] == model]
+        rs = [r for r in records if r["model"] == model and not r.get("no_aligned_grid")]
         s = {"gemms": len(rs), "fine_optimal": sum(not r["coarse_optimal"] for r in rs)}
         for name, _, _ in PLACEMENTS:
             if name == "ccl":
@@ -139,6 +148,9 @@ def markdown(records: list[dict]) -> str:
     lines = ["| GEMM | M×N×K | " + " | ".join(cols) + " | CCL grid | class |",
              "|" + "---|" * (len(cols) + 4)]
     for r in records:
+        if r.get("no_aligned_grid"):
+            lines.append(f"| {r['gemm']} | {r['M']}×{r['N']}×{r['K']} | no tile-aligned grid |")
+            continue
         ccl_b = r["ccl"]["remote_bytes"]
         cells = []
         for c in cols:
