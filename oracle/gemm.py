@@ -8,6 +8,8 @@ Precision: the paper evaluates BF16 GEMMs (Sec. IV-A). Reading: bf16
 operands, fp32 accumulation, bf16 output rounded to nearest even; the order
 of accumulation is free, so the GPU result is compared under a tolerance
 (relative Frobenius error <= 5e-3 and max abs error <= 1e-2 * max|C_ref|).
+Fig. 7 also sweeps the data type: fp8 (E4M3) operands and an fp32 output
+are decoded exactly here and compared the same way.
 
 Pinned by: integer (ternary) inputs against exact integer matmul, B = I,
 and per-element math.fsum on random inputs (tests).
@@ -23,12 +25,37 @@ def decode_bf16(bits: np.ndarray) -> np.ndarray:
     return b.view(np.float32).astype(np.float64)
 
 
+def decode_fp8_e4m3(bits: np.ndarray) -> np.ndarray:
+    """fp8 E4M3 bit patterns (uint8, the OCP 8-bit format with 4 exponent
+    bits, bias 7, 3 mantissa bits, no infinities) -> exact float64 values.
+
+    Exponent field 0 is subnormal: mantissa * 2^-9. S.1111.111 is NaN; every
+    other pattern, including exponent 15, is finite (largest 448).
+    """
+    b = np.asarray(bits, dtype=np.uint8).astype(np.int64)
+    sign = np.where(b & 0x80, -1.0, 1.0)
+    ex = (b >> 3) & 0xF
+    man = b & 0x7
+    val = np.where(ex == 0, man * 2.0 ** -9, (1.0 + man / 8.0) * np.exp2(ex - 7.0))
+    val = np.where((ex == 15) & (man == 7), np.nan, val)
+    return sign * val
+
+
+def decode(bits: np.ndarray) -> np.ndarray:
+    """Exact float64 values of bf16 (uint16) or fp8 E4M3 (uint8) bit arrays;
+    float arrays pass through."""
+    if bits.dtype == np.uint16:
+        return decode_bf16(bits)
+    if bits.dtype == np.uint8:
+        return decode_fp8_e4m3(bits)
+    return np.asarray(bits, dtype=np.float64)
+
+
 def gemm_fp64(A: np.ndarray, B: np.ndarray) -> np.ndarray:
-    """C = A B in float64. A, B are float64 (or bf16 bits as uint16)."""
-    if A.dtype == np.uint16:
-        A = decode_bf16(A)
-    if B.dtype == np.uint16:
-        B = decode_bf16(B)
+    """C = A B in float64. A, B are float64, bf16 bits (uint16) or fp8 E4M3
+    bits (uint8)."""
+    A = decode(A)
+    B = decode(B)
     if A.shape[1] != B.shape[0]:
         raise ValueError("inner dimensions differ")
     return A @ B
@@ -43,9 +70,7 @@ def gemm_scaled_fp64(A, B, C, alpha: float, beta: float) -> np.ndarray:
     P = gemm_fp64(A, B)
     if beta == 0:
         return alpha * P
-    if C.dtype == np.uint16:
-        C = decode_bf16(C)
-    return alpha * P + beta * C
+    return alpha * P + beta * decode(C)
 
 
 def gemm_entries(A: np.ndarray, B: np.ndarray, rows: np.ndarray, cols: np.ndarray) -> np.ndarray:
@@ -54,10 +79,8 @@ def gemm_entries(A: np.ndarray, B: np.ndarray, rows: np.ndarray, cols: np.ndarra
     A holds only the rows needed (indexed by rows), B is K x N (both may be
     bf16 bits). Used where the full product is too large for the host.
     """
-    if A.dtype == np.uint16:
-        A = decode_bf16(A)
-    if B.dtype == np.uint16:
-        B = decode_bf16(B)
+    A = decode(A)
+    B = decode(B)
     return np.einsum("ik,ki->i", A[rows], B[:, cols])
 
 

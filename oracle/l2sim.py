@@ -52,7 +52,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import layout
-from .plan import TILE, owner
+from .plan import TILE, elem_sizes, owner
 
 RR, COARSE, CCL = "rr", "coarse", "ccl"
 OPS = ("A", "B", "C")
@@ -160,8 +160,11 @@ def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
       misses[A, B]    of which missed
       remote[A, B, C] bytes: remote misses * line (A, B), remote C line writes
       remote_per_chiplet[G]  charged to the chiplet running the tile
+    e: element bytes, one for all operands or (e_A, e_B, e_C).
     """
     G = Gr * Gc
+    ea, eb, ec = elem_sizes(e)
+    esz = {"A": ea, "B": eb, "C": ec}
     nk = -(-K // k_step)
     acc = {"A": 0, "B": 0}
     mis = {"A": 0, "B": 0}
@@ -181,7 +184,7 @@ def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
                     n = range(tj * TILE, (tj + 1) * TILE)
                     for op, rows, cols in (("A", m, ks), ("B", ks, n)):
                         lines, homes = _slice_lines(op, rows, cols, M, N, K, Gr, Gc, P,
-                                                    placement, trans[op], e, line)
+                                                    placement, trans[op], esz[op], line)
                         for ln, h in zip(lines, homes):
                             acc[op] += 1
                             if not cache.access(ln):
@@ -192,7 +195,7 @@ def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
             for ti, tj in wave:
                 lines, homes = _slice_lines("C", range(ti * TILE, (ti + 1) * TILE),
                                             range(tj * TILE, (tj + 1) * TILE),
-                                            M, N, K, Gr, Gc, P, placement, 0, e, line)
+                                            M, N, K, Gr, Gc, P, placement, 0, ec, line)
                 for h in homes:
                     if h != p:
                         for _ in range(2 if c_read else 1):

@@ -25,8 +25,18 @@ Readings (the paper does not write these out):
 from __future__ import annotations
 
 TILE = 128          # model output tile, Sec. IV-A
-ELEM_BYTES = 2      # bf16 (Sec. IV-A "36 BF16 GEMMs")
+ELEM_BYTES = 2      # bf16 (Sec. IV-A: BF16 GEMMs)
 N_XCD = 8
+
+
+def elem_sizes(e) -> tuple[int, int, int]:
+    """Element bytes of (A, B, C): one int for all three, or a 3-tuple
+    (Fig. 7 sweeps the data type; fp8 operands with a bf16 or fp32 output
+    give different sizes per operand)."""
+    if isinstance(e, (tuple, list)):
+        ea, eb, ec = e
+        return int(ea), int(eb), int(ec)
+    return int(e), int(e), int(e)
 
 
 def is_pow2(x: int) -> bool:
@@ -49,32 +59,35 @@ def owner(ti: int, tj: int, M: int, N: int, Gr: int, Gc: int) -> int:
     return (ti // tiles_r) * Gc + (tj // tiles_c)
 
 
-def floor_bytes(M: int, N: int, K: int, Gr: int, Gc: int, e: int = ELEM_BYTES) -> int:
+def floor_bytes(M: int, N: int, K: int, Gr: int, Gc: int, e=ELEM_BYTES) -> int:
     """Lower bound on remote bytes of any layout under this ownership.
 
     Each A element is read by the Gc chiplets of its grid row, N/(Gc*128)
     times by each; at most one of them holds it, so (Gc-1)/Gc of its reads are
     remote. Same for B with Gr. C writes can all be local.
-    Integer form of e*M*N*K*[(Gc-1)/(Gc*128) + (Gr-1)/(Gr*128)].
+    Integer form of e*M*N*K*[(Gc-1)/(Gc*128) + (Gr-1)/(Gr*128)] (with e_A
+    and e_B for the two terms when the operands differ in size).
     """
-    a = e * M * K * (N // (Gc * TILE)) * (Gc - 1)
-    b = e * K * N * (M // (Gr * TILE)) * (Gr - 1)
+    ea, eb, _ = elem_sizes(e)
+    a = ea * M * K * (N // (Gc * TILE)) * (Gc - 1)
+    b = eb * K * N * (M // (Gr * TILE)) * (Gr - 1)
     return a + b
 
 
-def shared_replica_bytes(M: int, N: int, K: int, Gr: int, Gc: int, e: int = ELEM_BYTES) -> float:
+def shared_replica_bytes(M: int, N: int, K: int, Gr: int, Gc: int, e=ELEM_BYTES) -> float:
     """Bytes of each shared operand that its non-owning sharers also need."""
-    return e * (M * K * (Gc - 1) / Gc + K * N * (Gr - 1) / Gr)
+    ea, eb, _ = elem_sizes(e)
+    return ea * M * K * (Gc - 1) / Gc + eb * K * N * (Gr - 1) / Gr
 
 
-def auto_grid_rows(M: int, N: int, K: int, G: int) -> int:
+def auto_grid_rows(M: int, N: int, K: int, G: int, e=ELEM_BYTES) -> int:
     """Grid chosen for grid_rows = 0; 0 if no tile-aligned grid exists."""
     best = None
     for Gr in range(1, G + 1):
         if not grid_valid(M, N, K, G, Gr):
             continue
         Gc = G // Gr
-        key = (floor_bytes(M, N, K, Gr, Gc), shared_replica_bytes(M, N, K, Gr, Gc), Gr)
+        key = (floor_bytes(M, N, K, Gr, Gc, e), shared_replica_bytes(M, N, K, Gr, Gc, e), Gr)
         if best is None or key < best[0]:
             best = (key, Gr)
     return 0 if best is None else best[1]

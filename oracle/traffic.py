@@ -39,7 +39,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import layout
-from .plan import TILE, owner, floor_bytes
+from .plan import TILE, elem_sizes, owner, floor_bytes
 
 RR, COARSE, CCL = "rr", "coarse", "ccl"
 PLACEMENTS = (RR, COARSE, CCL)
@@ -76,11 +76,14 @@ def _hist(chips: np.ndarray, G: int) -> np.ndarray:
 def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2, c_read=False):
     """Remote bytes of C = A B (or alpha A B + beta C with c_read) under one placement.
 
+    e: element bytes, one for all operands or (e_A, e_B, e_C).
+
     Returns a dict of Python ints:
       accessed[A,B,C], remote[A,B,C], remote_per_chiplet[G],
       floor, footprint[A,B,C] (bytes of each stored operand, padding included).
     """
     G = Gr * Gc
+    ea, eb, ec = elem_sizes(e)
     TM, TN = M // TILE, N // TILE
     own = np.array([[owner(ti, tj, M, N, Gr, Gc) for tj in range(TN)] for ti in range(TM)],
                    dtype=np.int64)
@@ -91,20 +94,20 @@ def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2, c_rea
     cols = np.arange(K)
     for ti in range(TM):
         rows = np.arange(ti * TILE, (ti + 1) * TILE)
-        h = _hist(chip_of(rows[:, None], cols[None, :], M, K, trans_a, placement, Gr, Gc, P, e), G)
+        h = _hist(chip_of(rows[:, None], cols[None, :], M, K, trans_a, placement, Gr, Gc, P, ea), G)
         for tj in range(TN):
             o = own[ti, tj]
-            rb = e * (TILE * K - int(h[o]))
+            rb = ea * (TILE * K - int(h[o]))
             remote["A"] += rb
             per_chip[o] += rb
     # B column panels: panel tj holds K*TILE elements; every tile in column tj reads it.
     rows = np.arange(K)
     for tj in range(TN):
         cols = np.arange(tj * TILE, (tj + 1) * TILE)
-        h = _hist(chip_of(rows[:, None], cols[None, :], K, N, trans_b, placement, Gr, Gc, P, e), G)
+        h = _hist(chip_of(rows[:, None], cols[None, :], K, N, trans_b, placement, Gr, Gc, P, eb), G)
         for ti in range(TM):
             o = own[ti, tj]
-            rb = e * (K * TILE - int(h[o]))
+            rb = eb * (K * TILE - int(h[o]))
             remote["B"] += rb
             per_chip[o] += rb
     # C tiles: each written once by its owner (C is never stored transposed),
@@ -113,19 +116,20 @@ def remote_bytes(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, e=2, c_rea
     cols = np.arange(N)
     for ti in range(TM):
         rows = np.arange(ti * TILE, (ti + 1) * TILE)
-        ch = chip_of(rows[:, None], cols[None, :], M, N, 0, placement, Gr, Gc, P, e)
+        ch = chip_of(rows[:, None], cols[None, :], M, N, 0, placement, Gr, Gc, P, ec)
         ch = ch.reshape(TILE, TN, TILE).transpose(1, 0, 2).reshape(TN, -1)
         for tj in range(TN):
             o = own[ti, tj]
-            rb = c_times * e * int(np.count_nonzero(ch[tj] != o))
+            rb = c_times * ec * int(np.count_nonzero(ch[tj] != o))
             remote["C"] += rb
             per_chip[o] += rb
 
-    accessed = {"A": e * M * K * TN, "B": e * K * N * TM, "C": c_times * e * M * N}
+    accessed = {"A": ea * M * K * TN, "B": eb * K * N * TM, "C": c_times * ec * M * N}
+    esz = {"A": ea, "B": eb, "C": ec}
     if placement == CCL:
-        fp = {op: layout.total_bytes(*layout.operand_shape(op, M, N, K), Gr, Gc, P, e) for op in OPS}
+        fp = {op: layout.total_bytes(*layout.operand_shape(op, M, N, K), Gr, Gc, P, esz[op]) for op in OPS}
     else:
-        fp = {op: e * int(np.prod(layout.operand_shape(op, M, N, K))) for op in OPS}
+        fp = {op: esz[op] * int(np.prod(layout.operand_shape(op, M, N, K))) for op in OPS}
     return {
         "accessed": [accessed[o] for o in OPS],
         "remote": [int(remote[o]) for o in OPS],

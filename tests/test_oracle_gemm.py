@@ -93,3 +93,34 @@ def test_scaled_gemm_identity_a():
     eye = np.eye(64)
     got = O.gemm_scaled_fp64(eye, B, C, 0.25, -3.0)
     assert np.array_equal(got, 0.25 * O.decode_bf16(B) - 3.0 * O.decode_bf16(C))
+
+
+def test_fp8_decode_hand_values():
+    # 1.0 = 0.0111.000, -2.0 = 1.1000.000, 448 = 0.1111.110 (largest),
+    # 2^-6 = 0.0001.000 (smallest normal), 2^-9 = 0.0000.001 (smallest subnormal),
+    # 0.875 * 2^-6 = 0.0000.111, 1.125 = 0.0111.001
+    bits = np.array([0x38, 0xC0, 0x7E, 0x08, 0x01, 0x07, 0x39, 0x00, 0x80], dtype=np.uint8)
+    want = [1.0, -2.0, 448.0, 2.0 ** -6, 2.0 ** -9, 7 * 2.0 ** -9, 1.125, 0.0, -0.0]
+    got = O.decode_fp8_e4m3(bits)
+    assert list(got) == want
+    assert np.signbit(got[-1])
+    assert np.isnan(O.decode_fp8_e4m3(np.array([0x7F, 0xFF], dtype=np.uint8))).all()
+
+
+def test_fp8_decode_matches_torch_for_every_pattern():
+    torch = pytest.importorskip("torch")
+    bits = np.arange(256, dtype=np.uint8)
+    want = torch.from_numpy(bits).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = O.decode_fp8_e4m3(bits)
+    both_nan = np.isnan(want) & np.isnan(got)
+    assert np.array_equal(got[~both_nan], want[~both_nan])
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+
+
+def test_fp8_gemm_on_integers_is_exact():
+    A = W.draw_array_fp8(91, 48, 128, "ternary")
+    B = W.draw_array_fp8(92, 128, 40, "ternary")
+    ai = O.decode_fp8_e4m3(A).astype(np.int64)
+    bi = O.decode_fp8_e4m3(B).astype(np.int64)
+    assert set(np.unique(ai)) <= {-1, 0, 1}
+    assert np.array_equal(O.gemm_fp64(A, B), (ai @ bi).astype(np.float64))

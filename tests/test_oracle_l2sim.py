@@ -250,3 +250,15 @@ def test_c_read_is_charged_like_the_write(placement):
     assert read["remote"][:2] == plain["remote"][:2]
     assert read["remote"][2] == 2 * plain["remote"][2]
     assert read["misses"] == plain["misses"]
+
+
+@pytest.mark.parametrize("placement", PLACEMENTS)
+@pytest.mark.parametrize("e,k_step", [((1, 1, 2), 128), ((1, 1, 4), 128), ((2, 2, 4), 64),
+                                      ((4, 4, 4), 32)])
+def test_element_sizes_capacity_zero_is_tile_charge(placement, e, k_step):
+    """With a K step of one line per row (128 / e_A elements) the no-cache
+    limit still equals the tile-charge model for every element size."""
+    M, N, K, Gr, Gc, P = 256, 512, 512, 2, 2, 4096
+    ref = T.remote_bytes(M, N, K, Gr, Gc, P, placement, 1, 0, e=e)
+    got = L.simulate(M, N, K, Gr, Gc, P, placement, 1, 0, l2_bytes=0, slots=2, k_step=k_step, e=e)
+    assert got["remote"] == ref["remote"]

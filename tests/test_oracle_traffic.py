@@ -60,10 +60,11 @@ def _chip_matrix(R, Cc, trans, placement, Gr, Gc, P, e=2):
 
 def brute_remote(M, N, K, Gr, Gc, P, placement, ta=0, tb=0, chips=None, e=2, c_read=False):
     G = Gr * Gc
+    es = e if isinstance(e, tuple) else (e, e, e)
     if chips is None:
-        chips = (_chip_matrix(M, K, ta, placement, Gr, Gc, P),
-                 _chip_matrix(K, N, tb, placement, Gr, Gc, P),
-                 _chip_matrix(M, N, 0, placement, Gr, Gc, P))
+        chips = (_chip_matrix(M, K, ta, placement, Gr, Gc, P, es[0]),
+                 _chip_matrix(K, N, tb, placement, Gr, Gc, P, es[1]),
+                 _chip_matrix(M, N, 0, placement, Gr, Gc, P, es[2]))
     chA, chB, chC = chips
     remote = [0, 0, 0]
     accessed = [0, 0, 0]
@@ -77,9 +78,9 @@ def brute_remote(M, N, K, Gr, Gc, P, placement, ta=0, tb=0, chips=None, e=2, c_r
             if c_read:                          # beta != 0: the C tile is read too
                 blocks.append((2, chC[m0:m0 + 128, n0:n0 + 128]))
             for i, blk in blocks:
-                nb = e * int(np.count_nonzero(blk != own))
+                nb = es[i] * int(np.count_nonzero(blk != own))
                 remote[i] += nb
-                accessed[i] += e * blk.size
+                accessed[i] += es[i] * blk.size
                 per[own] += nb
     return remote, accessed, per
 
@@ -118,6 +119,23 @@ def test_c_read_equals_brute_force(M, N, K, Gr, Gc, P, ta, tb, placement):
     assert rec["accessed"] == accessed
     assert rec["remote_per_chiplet"] == per
     assert rec["accessed"][2] == 2 * 2 * M * N
+
+
+@pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", CASES[:6])
+@pytest.mark.parametrize("placement", T.PLACEMENTS)
+@pytest.mark.parametrize("e", [(1, 1, 2), (1, 1, 4), (2, 2, 4), (4, 4, 4)])
+def test_element_sizes_equal_brute_force(M, N, K, Gr, Gc, P, ta, tb, placement, e):
+    """fp8 / bf16 / fp32 operands (Fig. 7 data-type sweep): the page an
+    element lands on depends on its byte size."""
+    rec = T.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb, e=e)
+    remote, accessed, per = brute_remote(M, N, K, Gr, Gc, P, placement, ta, tb, e=e)
+    assert rec["remote"] == remote
+    assert rec["accessed"] == accessed
+    assert rec["remote_per_chiplet"] == per
+    if placement == "ccl":
+        ea, eb, _ = e
+        assert sum(rec["remote"]) == rec["floor"] == round(
+            M * N * K * (ea * (Gc - 1) / (Gc * 128) + eb * (Gr - 1) / (Gr * 128)))
 
 
 @pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", CASES)

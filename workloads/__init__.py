@@ -177,6 +177,30 @@ def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
 
 
+def round_to_fp8_e4m3_bits(x: np.ndarray) -> np.ndarray:
+    """float32 array -> uint8 fp8 E4M3 (OCP) bit patterns, round to nearest
+    even (torch's conversion). Draws stay far inside the +-448 range."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def draw_array_fp8(seed: int, rows: int, cols: int, dist: str = "normal", scale: float = 1.0) -> np.ndarray:
+    """Draw an ad-hoc (rows x cols) fp8 E4M3 bit array: the same float32 draw
+    as draw_array, rounded to fp8 instead of bf16."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = rows * cols
+    if dist == "uniform":
+        x = rng.uniform(-scale, scale, size=n).astype(np.float32)
+    elif dist == "normal":
+        x = rng.standard_normal(size=n, dtype=np.float32) * np.float32(scale)
+    elif dist == "ternary":
+        x = rng.integers(-1, 2, size=n).astype(np.float32)
+    else:
+        raise ValueError(dist)
+    return round_to_fp8_e4m3_bits(x).reshape(rows, cols)
+
+
 def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     """Exact widening of bf16 bit patterns to float64."""
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
