@@ -13,8 +13,10 @@
  *     locality-aware placement and CCL, Sec. IV-A.
  *
  * Conventions for every call:
- *   - Element type is bfloat16 (2 bytes) for A, B and C (Sec. IV-A: BF16
- *     GEMMs). Device buffers are passed as plain device pointers.
+ *   - Element types are the plan's: bfloat16 (2 bytes) for A, B and C with
+ *     ccl_plan (Sec. IV-A: BF16 GEMMs); ccl_plan_typed also takes fp8 E4M3
+ *     A and B and an fp32 C (Fig. 7 data types). e below is the element
+ *     size in bytes. Device buffers are passed as plain device pointers.
  *   - Logical operands are row-major: A is M x K, B is K x N, C is M x N.
  *   - The caller owns every buffer and the stream. The library allocates no
  *     device memory. A plan is owned by the caller from ccl_plan() until
@@ -31,8 +33,8 @@
  * is laid over each operand's own rows and columns: A is split along K by
  * Gc, B along K by Gr):
  *   hr = R / Gr, wc = Cc / Gc, block b(r, c) = (r / hr) * Gc + c / wc,
- *   strip bytes S = ceil(hr * wc * 2 / page) * page,
- *   byte offset(r, c) = b * S + ((r % hr) * wc + c % wc) * 2.
+ *   strip bytes S = ceil(hr * wc * e / page) * page,
+ *   byte offset(r, c) = b * S + ((r % hr) * wc + c % wc) * e.
  * Block b lives on chiplet b. With Gr = 1 and no padding this is Eq. 3.
  * Padding bytes at the end of each strip are never read or written.
  */
@@ -58,6 +60,13 @@ typedef enum {
 
 typedef enum { CCL_A = 0, CCL_B = 1, CCL_C = 2 } ccl_operand;
 
+/* Element types (Fig. 7 sweeps the data type). A and B share one type. */
+typedef enum {
+  CCL_DT_BF16 = 0,       /* 2 bytes */
+  CCL_DT_FP8_E4M3 = 1,   /* 1 byte: OCP 8-bit float, 4 exponent bits (bias 7), 3 mantissa bits */
+  CCL_DT_FP32 = 2        /* 4 bytes (C only) */
+} ccl_dtype;
+
 typedef enum {
   CCL_PLACE_RR = 0,      /* fixed-size pages to chiplets round-robin (Sec. IV-A) */
   CCL_PLACE_COARSE = 1,  /* G contiguous page-granular chunks (Sec. IV-A, Coarse LA) */
@@ -72,6 +81,7 @@ typedef struct {
   int64_t strip_bytes;           /* block_rows * block_cols * 2 */
   int64_t strip_stride_bytes;    /* strip_bytes rounded up to the page */
   int64_t total_bytes;           /* grid_r * grid_c * strip_stride_bytes: buffer size */
+  int64_t elem_bytes;            /* bytes per element: 1 (fp8), 2 (bf16) or 4 (fp32) */
 } ccl_layout;
 
 #define CCL_MAX_CHIPLETS 64
@@ -97,6 +107,7 @@ typedef struct {
  * partitioning per GEMM): the tile-aligned grid with the fewest CCL remote
  * bytes, then the one whose shared operands replicate fewer bytes, then the
  * smaller grid_rows.
+ * All three operands are bf16 (ccl_plan_typed with CCL_DT_BF16, CCL_DT_BF16).
  * Errors: CCL_ERR_INVALID_ARG (non-positive size, chiplets out of range,
  * grid_rows not dividing chiplets, bad page, out == NULL, size overflow);
  * CCL_ERR_UNALIGNED_PARTITION (M % (Gr*128), N % (Gc*128), K % Gr or
@@ -104,6 +115,19 @@ typedef struct {
  */
 ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
                     int64_t page_bytes, ccl_plan_t* out);
+
+/*
+ * ccl_plan with element types: ab_type for A and B (CCL_DT_BF16 or
+ * CCL_DT_FP8_E4M3), c_type for C (CCL_DT_BF16 or CCL_DT_FP32). The element
+ * size sets the strip bytes and padding of each layout and the bytes of the
+ * traffic models (Sec. II-B: the slice a chiplet needs is N/G elements, so
+ * its byte size depends on the type). The automatic grid weighs A and B by
+ * their element size. Errors as ccl_plan; CCL_ERR_INVALID_ARG also for
+ * other type combinations.
+ */
+ccl_status ccl_plan_typed(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
+                          int64_t page_bytes, ccl_dtype ab_type, ccl_dtype c_type,
+                          ccl_plan_t* out);
 
 /* Release a plan. NULL is accepted. */
 ccl_status ccl_plan_destroy(ccl_plan_t plan);
@@ -119,6 +143,7 @@ ccl_status ccl_plan_layout(ccl_plan_t plan, ccl_operand op, ccl_layout* out);
  * activations repacked). src_trans = 0: src is the row-major operand
  * (rows x cols, leading dimension ld >= cols elements). src_trans = 1: src
  * holds the transpose (cols x rows, ld >= rows), e.g. H for A = H^T.
+ * Elements are the operand's type (bit copies, any of the three types).
  * dst_ccl has ccl_plan_layout().total_bytes bytes; padding is not written.
  * Errors: CCL_ERR_INVALID_ARG (null pointer, op not A/B/C, ld too small,
  * src_trans on C); CCL_ERR_HIP.
@@ -136,14 +161,14 @@ ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void
 
 /*
  * C_ccl = A_ccl B_ccl, all three in the plan's CCL layouts: bf16 inputs,
- * fp32 accumulation on the matrix cores, bf16 output rounded to nearest
- * even (Sec. II-B, III-C). Each XCD computes exactly the output tiles of
+ * fp32 accumulation on the matrix cores, output rounded to nearest even to
+ * bf16 or stored as fp32, per the plan's C type (Sec. II-B, III-C). Each XCD computes exactly the output tiles of
  * the partition its chiplet owns (chiplet c <-> XCDs c*8/G .. c*8/G+8/G-1),
  * so chiplets must divide 8.
  * Errors: CCL_ERR_INVALID_ARG (null pointer); CCL_ERR_MISALIGNED_POINTER
  * (pointer not 16-byte aligned); CCL_ERR_UNSUPPORTED (chiplets not dividing
- * 8, K / Gc or K / Gr not a multiple of 32, device not gfx950);
- * CCL_ERR_HIP.
+ * 8, K / Gc or K / Gr not a multiple of 32, A and B not bf16, device not
+ * gfx950); CCL_ERR_HIP.
  */
 ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
                     void* stream);
@@ -152,8 +177,8 @@ ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void*
  * C_ccl = alpha * A_ccl B_ccl + beta * C_ccl, the BLAS form of the GEMM
  * (Sec. II-B): the scalars change no placement, and each output tile's owner
  * reads its C tile where it writes it. The product is accumulated in fp32,
- * then alpha * acc + beta * c is formed in fp32 and rounded to bf16 (nearest
- * even). beta == 0: C is not read (its old contents, NaN included, do not
+ * then alpha * acc + beta * c is formed in fp32 and stored in C's type
+ * (bf16: nearest even). beta == 0: C is not read (its old contents, NaN included, do not
  * matter), as in BLAS. ccl_gemm is alpha = 1, beta = 0.
  * Errors as ccl_gemm.
  */

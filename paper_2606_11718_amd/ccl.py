@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
                 3: "CCL_ERR_UNSUPPORTED", 4: "CCL_ERR_MISALIGNED_POINTER", 5: "CCL_ERR_HIP"}
 
 # every symbol include/ccl.h declares
-EXPORTED = ("ccl_plan", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
+EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
             "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
@@ -38,7 +38,7 @@ class CCLError(RuntimeError):
 class _Layout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in ("rows", "cols", "grid_r", "grid_c", "block_rows",
                                                "block_cols", "strip_bytes", "strip_stride_bytes",
-                                               "total_bytes")]
+                                               "total_bytes", "elem_bytes")]
 
 
 class _Traffic(ctypes.Structure):
@@ -79,6 +79,7 @@ def library() -> ctypes.CDLL:
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
     sig = {
         "ccl_plan": [i64, i64, i64, i32, i32, i64, ctypes.POINTER(vp)],
+        "ccl_plan_typed": [i64, i64, i64, i32, i32, i64, i32, i32, ctypes.POINTER(vp)],
         "ccl_plan_destroy": [vp],
         "ccl_plan_grid": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "ccl_plan_layout": [vp, i32, ctypes.POINTER(_Layout)],
@@ -158,12 +159,24 @@ class Layout:
     strip_bytes: int
     strip_stride_bytes: int
     total_bytes: int
+    elem_bytes: int
+
+
+CCL_DT_BF16, CCL_DT_FP8_E4M3, CCL_DT_FP32 = 0, 1, 2
 
 
 def ccl_plan(M: int, N: int, K: int, chiplets: int, grid_rows: int, page_bytes: int) -> Plan:
     h = ctypes.c_void_p()
     _check(library().ccl_plan(M, N, K, chiplets, grid_rows, page_bytes, ctypes.byref(h)))
     return Plan(h.value, (M, N, K, chiplets, grid_rows, page_bytes))
+
+
+def ccl_plan_typed(M: int, N: int, K: int, chiplets: int, grid_rows: int, page_bytes: int,
+                   ab_type: int, c_type: int) -> Plan:
+    h = ctypes.c_void_p()
+    _check(library().ccl_plan_typed(M, N, K, chiplets, grid_rows, page_bytes, ab_type, c_type,
+                                    ctypes.byref(h)))
+    return Plan(h.value, (M, N, K, chiplets, grid_rows, page_bytes, ab_type, c_type))
 
 
 def ccl_plan_grid(plan: Plan) -> tuple[int, int]:

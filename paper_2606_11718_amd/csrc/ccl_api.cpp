@@ -63,12 +63,12 @@ ccl_status hip_status(hipError_t e, const char* what) {
 
 bool valid_op(ccl_operand op) { return op == CCL_A || op == CCL_B || op == CCL_C; }
 
-// CCL addressing of the GEMM operands (elements).
+// CCL addressing of the GEMM operands (in elements of each operand's type).
 void ccl_addressing(const ccl::Plan& p, ccl::OperandAddr* a, ccl::OperandAddr* b,
                     ccl::OperandAddr* c) {
-  const int64_t sa = p.lay[ccl::OP_A].strip_stride_bytes / 2;
-  const int64_t sb = p.lay[ccl::OP_B].strip_stride_bytes / 2;
-  const int64_t sc = p.lay[ccl::OP_C].strip_stride_bytes / 2;
+  const int64_t sa = p.lay[ccl::OP_A].strip_stride_bytes / p.lay[ccl::OP_A].elem_bytes;
+  const int64_t sb = p.lay[ccl::OP_B].strip_stride_bytes / p.lay[ccl::OP_B].elem_bytes;
+  const int64_t sc = p.lay[ccl::OP_C].strip_stride_bytes / p.lay[ccl::OP_C].elem_bytes;
   // A block (pr, kc) = pr*Gc + kc; B block (kr, pc) = kr*Gc + pc; C block (pr, pc).
   *a = {p.Gc * sa, sa, (int32_t)(p.K / p.Gc), (int32_t)(p.K / p.Gc)};
   *b = {sb, p.Gc * sb, (int32_t)(p.N / p.Gc), (int32_t)(p.K / p.Gr)};
@@ -85,6 +85,23 @@ void rowmajor_addressing(const ccl::Plan& p, ccl::OperandAddr* a, ccl::OperandAd
   *c = {hr * p.N, p.N / p.Gc, (int32_t)p.N, 0};
 }
 
+// Whether every element the GEMM kernel can touch through this addressing
+// lies inside buffers of a_bytes, b_bytes and c_bytes (the kernel's own
+// formulas: A at pr*part + kslice_index*slice + row*ld + k, B at
+// pc*part + kslice_index*slice + k*ld + n, C at pr*part + pc*slice +
+// row*ld + n).
+bool addressing_in_bounds(const ccl::Plan& p, const ccl::OperandAddr& a, const ccl::OperandAddr& b,
+                          const ccl::OperandAddr& c, int64_t a_bytes, int64_t b_bytes,
+                          int64_t c_bytes) {
+  const int64_t hr = p.M / p.Gr, wc = p.N / p.Gc;
+  const int64_t a_end = (p.Gr - 1) * a.part + (p.K / a.kslice - 1) * a.slice + (hr - 1) * a.ld + a.kslice;
+  const int64_t b_end = (p.Gc - 1) * b.part + (p.K / b.kslice - 1) * b.slice + (b.kslice - 1) * b.ld + wc;
+  const int64_t c_end = (p.Gr - 1) * c.part + (p.Gc - 1) * c.slice + (hr - 1) * c.ld + wc;
+  return a_end * p.lay[ccl::OP_A].elem_bytes <= a_bytes &&
+         b_end * p.lay[ccl::OP_B].elem_bytes <= b_bytes &&
+         c_end * p.lay[ccl::OP_C].elem_bytes <= c_bytes;
+}
+
 // The kernel addresses a tile's K step with 32-bit byte offsets from its
 // corner: up to 255 rows of A and 31 rows of B.
 bool offsets_fit(const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
@@ -96,19 +113,26 @@ bool offsets_fit(const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
 
 extern "C" {
 
-ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
-                    int64_t page_bytes, ccl_plan_t* out) {
+ccl_status ccl_plan_typed(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
+                          int64_t page_bytes, ccl_dtype ab_type, ccl_dtype c_type, ccl_plan_t* out) {
   if (!out) return fail(CCL_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   ccl::Plan p;
   std::string err;
-  ccl::Status s = ccl::make_plan(M, N, K, chiplets, grid_rows, page_bytes, &p, &err);
+  ccl::Status s = ccl::make_plan(M, N, K, chiplets, grid_rows, page_bytes,
+                                 static_cast<ccl::DType>(ab_type), static_cast<ccl::DType>(c_type),
+                                 &p, &err);
   if (s != ccl::Status::OK) return from(s, err);
   ccl_plan_s* h = new (std::nothrow) ccl_plan_s;
   if (!h) return fail(CCL_ERR_INVALID_ARG, "out of host memory");
   h->plan = p;
   *out = h;
   return ok();
+}
+
+ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows,
+                    int64_t page_bytes, ccl_plan_t* out) {
+  return ccl_plan_typed(M, N, K, chiplets, grid_rows, page_bytes, CCL_DT_BF16, CCL_DT_BF16, out);
 }
 
 ccl_status ccl_plan_destroy(ccl_plan_t plan) {
@@ -136,6 +160,7 @@ ccl_status ccl_plan_layout(ccl_plan_t plan, ccl_operand op, ccl_layout* out) {
   out->strip_bytes = l.strip_bytes;
   out->strip_stride_bytes = l.strip_stride_bytes;
   out->total_bytes = l.total_bytes;
+  out->elem_bytes = l.elem_bytes;
   return ok();
 }
 
@@ -179,6 +204,9 @@ ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, cons
   ccl::OperandAddr a, b, c;
   ccl_addressing(p, &a, &b, &c);
   if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
+  if (!addressing_in_bounds(p, a, b, c, p.lay[ccl::OP_A].total_bytes, p.lay[ccl::OP_B].total_bytes,
+                            p.lay[ccl::OP_C].total_bytes))
+    return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the CCL buffers");
   if (ccl_status s = check_device()) return s;
   return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, alpha, beta,
                                      static_cast<hipStream_t>(stream)),
@@ -201,6 +229,10 @@ ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void
   ccl::OperandAddr a, b, c;
   rowmajor_addressing(p, &a, &b, &c);
   if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "rows too long for 32-bit in-tile offsets");
+  if (!addressing_in_bounds(p, a, b, c, p.M * p.K * p.lay[ccl::OP_A].elem_bytes,
+                            p.K * p.N * p.lay[ccl::OP_B].elem_bytes,
+                            p.M * p.N * p.lay[ccl::OP_C].elem_bytes))
+    return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the operands");
   if (ccl_status s = check_device()) return s;
   return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1, 1.f, 0.f,
                                      static_cast<hipStream_t>(stream)),

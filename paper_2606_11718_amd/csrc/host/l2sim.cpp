@@ -37,6 +37,7 @@ struct Stored {
   Placement place = PLACE_RR;
   int G = 1;
   int64_t page = 4096, n_pages = 1;
+  int64_t e = 2;                     // element bytes
   uint64_t base_line = 0;            // line number of the buffer's first byte
 
   int home(int64_t off) const {
@@ -55,6 +56,7 @@ Stored make_stored(const Plan& p, Op op, Placement pl, bool trans, int line) {
   s.place = pl;
   s.G = p.G;
   s.page = p.page;
+  s.e = L.elem_bytes;
   if (pl == PLACE_CCL) {
     s.kind = CCL_STRIPS;
     s.hr = L.block_rows;
@@ -63,7 +65,7 @@ Stored make_stored(const Plan& p, Op op, Placement pl, bool trans, int line) {
     s.S = L.strip_stride_bytes;
   } else {
     s.kind = trans ? TRANSPOSED : ROW_MAJOR;
-    s.n_pages = (L.rows * L.cols * kElemBytes + p.page - 1) / p.page;
+    s.n_pages = (L.rows * L.cols * L.elem_bytes + p.page - 1) / p.page;
   }
   s.base_line = (uint64_t(op) << 40) / uint64_t(line);   // A at 0, B at 2^40, C at 2^41
   return s;
@@ -84,7 +86,7 @@ void for_each_line(const Stored& s, int64_t r0, int64_t r1, int64_t c0, int64_t 
     for (; l <= l1; ++l) f(l << line_shift);
     last = l1;
   };
-  const int64_t e = kElemBytes;
+  const int64_t e = s.e;
   switch (s.kind) {
     case ROW_MAJOR:
       for (int64_t r = r0; r < r1; ++r) run((r * s.C + c0) * e, (r * s.C + c1) * e);

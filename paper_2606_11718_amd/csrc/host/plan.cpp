@@ -21,26 +21,27 @@ namespace {
 
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
-Layout make_layout(int64_t rows, int64_t cols, int Gr, int Gc, int64_t page) {
+Layout make_layout(int64_t rows, int64_t cols, int Gr, int Gc, int64_t page, int e) {
   Layout l;
+  l.elem_bytes = e;
   l.rows = rows;
   l.cols = cols;
   l.grid_r = Gr;
   l.grid_c = Gc;
   l.block_rows = rows / Gr;
   l.block_cols = cols / Gc;
-  l.strip_bytes = l.block_rows * l.block_cols * kElemBytes;
+  l.strip_bytes = l.block_rows * l.block_cols * e;
   l.strip_stride_bytes = (l.strip_bytes + page - 1) / page * page;
   l.total_bytes = l.strip_stride_bytes * Gr * Gc;
   return l;
 }
 
 // Extra bytes of the shared operands that their non-owning sharers need,
-// scaled by G to stay an integer: e*(M*K*(Gc-1)*Gr + K*N*(Gr-1)*Gc).
-unsigned __int128 replicated_times_g(int64_t M, int64_t N, int64_t K, int Gr, int Gc) {
-  unsigned __int128 a = (unsigned __int128)M * K * (Gc - 1) * Gr;
-  unsigned __int128 b = (unsigned __int128)K * N * (Gr - 1) * Gc;
-  return (a + b) * kElemBytes;
+// scaled by G to stay an integer: e_A*M*K*(Gc-1)*Gr + e_B*K*N*(Gr-1)*Gc.
+unsigned __int128 replicated_times_g(int64_t M, int64_t N, int64_t K, int Gr, int Gc, int ea, int eb) {
+  unsigned __int128 a = (unsigned __int128)M * K * (Gc - 1) * Gr * ea;
+  unsigned __int128 b = (unsigned __int128)K * N * (Gr - 1) * Gc * eb;
+  return a + b;
 }
 
 void choose_gemm_config(Plan* p) {
@@ -49,6 +50,10 @@ void choose_gemm_config(Plan* p) {
   const int64_t pr = p->part_rows(), pc = p->part_cols();
   if (kNumXcd % p->G != 0) {
     g.why_unsupported = "chiplets must divide the 8 XCDs";
+    return;
+  }
+  if (p->ab_type != DT_BF16) {
+    g.why_unsupported = "the GEMM kernels take bf16 A and B";
     return;
   }
   if ((p->K / p->Gc) % kGemmBK != 0 || (p->K / p->Gr) % kGemmBK != 0) {
@@ -112,6 +117,7 @@ struct Placed {
   int G;
   int64_t page;
   int64_t n_pages;    // pages of the stored row-major tensor
+  int64_t e;          // element bytes
 
   int chip_of_page(int64_t pg) const {
     if (pl == PLACE_RR) return (int)(pg % G);
@@ -123,7 +129,7 @@ struct Placed {
     int64_t pg = s0 / page;
     while (s0 < s1) {
       int64_t end = std::min((pg + 1) * page, s1);
-      h[chip_of_page(pg)] += (uint64_t)((end - s0) / kElemBytes);
+      h[chip_of_page(pg)] += (uint64_t)((end - s0) / e);
       s0 = end;
       ++pg;
     }
@@ -144,10 +150,10 @@ struct Placed {
     }
     if (!trans) {
       for (int64_t r = r0; r < r1; ++r)
-        add_interval((r * Cc + c0) * kElemBytes, (r * Cc + c1) * kElemBytes, h);
+        add_interval((r * Cc + c0) * e, (r * Cc + c1) * e, h);
     } else {
       for (int64_t c = c0; c < c1; ++c)
-        add_interval((c * R + r0) * kElemBytes, (c * R + r1) * kElemBytes, h);
+        add_interval((c * R + r0) * e, (c * R + r1) * e, h);
     }
   }
 };
@@ -161,15 +167,15 @@ bool grid_aligned(int64_t M, int64_t N, int64_t K, int G, int Gr) {
          K % Gr == 0 && K % Gc == 0;
 }
 
-uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc) {
+uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc, int ea, int eb) {
   // A: each element read by Gc chiplets, N/(Gc*128) times each, one of them local.
-  unsigned __int128 a = (unsigned __int128)M * K * (N / ((int64_t)Gc * kModelTile)) * (Gc - 1);
-  unsigned __int128 b = (unsigned __int128)K * N * (M / ((int64_t)Gr * kModelTile)) * (Gr - 1);
-  return (uint64_t)((a + b) * kElemBytes);
+  unsigned __int128 a = (unsigned __int128)M * K * (N / ((int64_t)Gc * kModelTile)) * (Gc - 1) * ea;
+  unsigned __int128 b = (unsigned __int128)K * N * (M / ((int64_t)Gr * kModelTile)) * (Gr - 1) * eb;
+  return (uint64_t)(a + b);
 }
 
 Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, int64_t page,
-                 Plan* out, std::string* err) {
+                 DType ab, DType c, Plan* out, std::string* err) {
   if (!out) {
     *err = "plan output pointer is NULL";
     return Status::INVALID_ARG;
@@ -195,6 +201,11 @@ Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, i
     *err = "page_bytes must be a power of two in [128, 2^40]";
     return Status::INVALID_ARG;
   }
+  if ((ab != DT_BF16 && ab != DT_FP8_E4M3) || (c != DT_BF16 && c != DT_FP32)) {
+    *err = "A and B must be bf16 or fp8 E4M3, C bf16 or fp32";
+    return Status::INVALID_ARG;
+  }
+  const int ea = dtype_bytes(ab), ec = dtype_bytes(c);
   if (grid_rows < 0 || (grid_rows > 0 && chiplets % grid_rows != 0)) {
     *err = "grid_rows must be 0 (automatic) or divide chiplets";
     return Status::INVALID_ARG;
@@ -208,8 +219,8 @@ Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, i
     unsigned __int128 best_rep = 0;
     for (int r = 1; r <= chiplets; ++r) {
       if (!grid_aligned(M, N, K, chiplets, r)) continue;
-      uint64_t f = floor_bytes(M, N, K, r, chiplets / r);
-      unsigned __int128 rep = replicated_times_g(M, N, K, r, chiplets / r);
+      uint64_t f = floor_bytes(M, N, K, r, chiplets / r, ea, ea);
+      unsigned __int128 rep = replicated_times_g(M, N, K, r, chiplets / r, ea, ea);
       if (!found || f < best_floor || (f == best_floor && rep < best_rep)) {
         found = true;
         best_floor = f;
@@ -233,9 +244,11 @@ Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, i
   p.Gr = Gr;
   p.Gc = chiplets / Gr;
   p.page = page;
-  p.lay[OP_A] = make_layout(M, K, p.Gr, p.Gc, page);
-  p.lay[OP_B] = make_layout(K, N, p.Gr, p.Gc, page);
-  p.lay[OP_C] = make_layout(M, N, p.Gr, p.Gc, page);
+  p.ab_type = ab;
+  p.c_type = c;
+  p.lay[OP_A] = make_layout(M, K, p.Gr, p.Gc, page, ea);
+  p.lay[OP_B] = make_layout(K, N, p.Gr, p.Gc, page, ea);
+  p.lay[OP_C] = make_layout(M, N, p.Gr, p.Gc, page, ec);
   choose_gemm_config(&p);
   *out = p;
   return Status::OK;
@@ -253,13 +266,14 @@ Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
   const int64_t shapes[3][2] = {{p.M, p.K}, {p.K, p.N}, {p.M, p.N}};
   Placed ops[3];
   for (int o = 0; o < 3; ++o) {
-    int64_t bytes = shapes[o][0] * shapes[o][1] * kElemBytes;
+    const int64_t e = p.lay[o].elem_bytes;
+    int64_t bytes = shapes[o][0] * shapes[o][1] * e;
     ops[o] = Placed{shapes[o][0], shapes[o][1], o < 2 && ((trans_mask >> o) & 1), pl,
-                    &p.lay[o],   G,            p.page, (bytes + p.page - 1) / p.page};
+                    &p.lay[o],   G,            p.page, (bytes + p.page - 1) / p.page, e};
     t.footprint[o] = pl == PLACE_CCL ? (uint64_t)p.lay[o].total_bytes : (uint64_t)bytes;
   }
   std::vector<uint64_t> h(G);
-  const uint64_t e = kElemBytes;
+  const uint64_t ea = p.lay[OP_A].elem_bytes, eb = p.lay[OP_B].elem_bytes, ec = p.lay[OP_C].elem_bytes;
 
   // A: row panel ti is read by the TN tiles of its row; the tiles of grid
   // column pc are owned by chiplet pr*Gc + pc, tn_per_part of them.
@@ -269,7 +283,7 @@ Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
     const int pr = (int)(ti / tm_per_part);
     for (int pc = 0; pc < p.Gc; ++pc) {
       const int o = pr * p.Gc + pc;
-      uint64_t rem = e * (uint64_t)tn_per_part * ((uint64_t)(T * p.K) - h[o]);
+      uint64_t rem = ea * (uint64_t)tn_per_part * ((uint64_t)(T * p.K) - h[o]);
       t.remote[OP_A] += rem;
       t.remote_per_chiplet[o] += rem;
     }
@@ -281,7 +295,7 @@ Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
     const int pc = (int)(tj / tn_per_part);
     for (int pr = 0; pr < p.Gr; ++pr) {
       const int o = pr * p.Gc + pc;
-      uint64_t rem = e * (uint64_t)tm_per_part * ((uint64_t)(p.K * T) - h[o]);
+      uint64_t rem = eb * (uint64_t)tm_per_part * ((uint64_t)(p.K * T) - h[o]);
       t.remote[OP_B] += rem;
       t.remote_per_chiplet[o] += rem;
     }
@@ -293,15 +307,15 @@ Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
       std::fill(h.begin(), h.end(), 0);
       ops[OP_C].count(ti * T, (ti + 1) * T, tj * T, (tj + 1) * T, h.data());
       const int o = p.owner(ti, tj);
-      uint64_t rem = c_times * e * ((uint64_t)(T * T) - h[o]);
+      uint64_t rem = c_times * ec * ((uint64_t)(T * T) - h[o]);
       t.remote[OP_C] += rem;
       t.remote_per_chiplet[o] += rem;
     }
   }
-  t.accessed[OP_A] = e * (uint64_t)p.M * p.K * TN;
-  t.accessed[OP_B] = e * (uint64_t)p.K * p.N * TM;
-  t.accessed[OP_C] = c_times * e * (uint64_t)p.M * p.N;
-  t.floor_bytes = floor_bytes(p.M, p.N, p.K, p.Gr, p.Gc);
+  t.accessed[OP_A] = ea * (uint64_t)p.M * p.K * TN;
+  t.accessed[OP_B] = eb * (uint64_t)p.K * p.N * TM;
+  t.accessed[OP_C] = c_times * ec * (uint64_t)p.M * p.N;
+  t.floor_bytes = floor_bytes(p.M, p.N, p.K, p.Gr, p.Gc, (int)ea, (int)eb);
   return t;
 }
 

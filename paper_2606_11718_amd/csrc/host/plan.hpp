@@ -11,12 +11,14 @@
 namespace ccl {
 
 constexpr int kModelTile = 128;   // output tile of the traffic model (Sec. IV-A)
-constexpr int kElemBytes = 2;     // bf16
 constexpr int kNumXcd = 8;        // MI355X: 8 XCDs, workgroups dispatched round-robin
 constexpr int kMaxChiplets = 64;
 constexpr int kGemmBK = 32;       // K extent of one GEMM main-loop step
 
 enum Op { OP_A = 0, OP_B = 1, OP_C = 2 };
+// Element types (Fig. 7 sweeps the data type): A and B share one type.
+enum DType { DT_BF16 = 0, DT_FP8_E4M3 = 1, DT_FP32 = 2 };
+inline int dtype_bytes(DType t) { return t == DT_FP8_E4M3 ? 1 : (t == DT_FP32 ? 4 : 2); }
 enum Placement { PLACE_RR = 0, PLACE_COARSE = 1, PLACE_CCL = 2 };
 
 struct Layout {
@@ -24,11 +26,12 @@ struct Layout {
   int64_t grid_r = 0, grid_c = 0;
   int64_t block_rows = 0, block_cols = 0;
   int64_t strip_bytes = 0, strip_stride_bytes = 0, total_bytes = 0;
+  int64_t elem_bytes = 2;
 
   // Byte offset of logical element (r, c) (Sec. III-B, block form of Eq. 3).
   int64_t offset(int64_t r, int64_t c) const {
     int64_t b = (r / block_rows) * grid_c + (c / block_cols);
-    return b * strip_stride_bytes + ((r % block_rows) * block_cols + (c % block_cols)) * kElemBytes;
+    return b * strip_stride_bytes + ((r % block_rows) * block_cols + (c % block_cols)) * elem_bytes;
   }
 };
 
@@ -58,6 +61,7 @@ struct Plan {
   int64_t M = 0, N = 0, K = 0;
   int G = 0, Gr = 0, Gc = 0;
   int64_t page = 0;
+  DType ab_type = DT_BF16, c_type = DT_BF16;
   Layout lay[3];
   GemmConfig gemm;
 
@@ -72,15 +76,17 @@ struct Plan {
 enum class Status { OK = 0, INVALID_ARG = 1, UNALIGNED = 2, UNSUPPORTED = 3, MISALIGNED = 4, HIP = 5 };
 
 // Build a plan. grid_rows == 0 chooses the grid. On error returns the status
-// and fills `err` with a message.
+// and fills `err` with a message. ab: type of A and B (bf16 or fp8 E4M3);
+// c: type of C (bf16 or fp32).
 Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, int64_t page,
-                 Plan* out, std::string* err);
+                 DType ab, DType c, Plan* out, std::string* err);
 
 // Whether a Gr x (G/Gr) grid gives tile-aligned partitions.
 bool grid_aligned(int64_t M, int64_t N, int64_t K, int G, int Gr);
 
-// Remote bytes of CCL (the floor): e*M*N*K*[(Gc-1)/(Gc*128) + (Gr-1)/(Gr*128)].
-uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc);
+// Remote bytes of CCL (the floor):
+// M*N*K*[e_A*(Gc-1)/(Gc*128) + e_B*(Gr-1)/(Gr*128)].
+uint64_t floor_bytes(int64_t M, int64_t N, int64_t K, int Gr, int Gc, int ea, int eb);
 
 // Traffic flags: bit 0 A stored transposed, bit 1 B stored transposed,
 // bit 2 C is read as well as written (alpha A B + beta C with beta != 0).

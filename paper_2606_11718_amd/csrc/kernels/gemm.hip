@@ -43,13 +43,14 @@ constexpr int kStages = 4;       // LDS stages; loads run kStages-1 steps ahead
 struct GemmParams {
   const uint16_t* A;
   const uint16_t* B;
-  uint16_t* C;
+  void* C;                // bf16, or fp32 when c_f32
   OperandAddr a, b, c;
   TileMap map;
   int32_t ksteps;       // K / 32
   int32_t remap;        // 1: XCD-aware map; 0: native raster over the whole C
   int32_t grid_r;       // Gr (native raster)
   int32_t epi;          // epilogue: 0 acc, 1 alpha*acc, 2 alpha*acc + beta*C (C read)
+  int32_t c_f32;        // C elements are fp32 (else bf16)
   float alpha, beta;
 };
 
@@ -344,9 +345,15 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   }
 
   // ---- epilogue: lane holds C[m][n .. n+3] for each (mt, nt, q) ----
-  uint16_t* c_tile = p.C + pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
   const int epi = p.epi;
   const float alpha = p.alpha, beta = p.beta;
+  // alpha * acc (+ beta * old) for the four values; old only read when epi == 2.
+  auto scale = [&](float* o, const float* old) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * old[j]) : alpha * o[j];
+  };
 #pragma unroll
   for (int mt = 0; mt < T::TM; ++mt) {
     const int m = wm * T::WM + mt * 32 + (lane & 31);
@@ -355,22 +362,35 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = wn * T::WN + nt * 32 + 8 * q + 4 * (lane >> 5);
-        uint2* dst = reinterpret_cast<uint2*>(c_tile + (int64_t)m * p.c.ld + n);
+        const int64_t idx = c_tile + (int64_t)m * p.c.ld + n;
         float o[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
-        if (epi != 0) {
-          uint2 old = make_uint2(0u, 0u);
-          if (epi == 2) old = *dst;
-          const float c[4] = {__uint_as_float(old.x << 16), __uint_as_float(old.x & 0xffff0000u),
-                              __uint_as_float(old.y << 16), __uint_as_float(old.y & 0xffff0000u)};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * c[j]) : alpha * o[j];
+        if (p.c_f32) {
+          float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.C) + idx);
+          if (epi != 0) {
+            float old[4] = {0.f, 0.f, 0.f, 0.f};
+            if (epi == 2) {
+              const float4 c = *dst;
+              old[0] = c.x; old[1] = c.y; old[2] = c.z; old[3] = c.w;
+            }
+            scale(o, old);
+          }
+          *dst = make_float4(o[0], o[1], o[2], o[3]);
+        } else {
+          uint2* dst = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.C) + idx);
+          if (epi != 0) {
+            uint2 c = make_uint2(0u, 0u);
+            if (epi == 2) c = *dst;
+            const float old[4] = {__uint_as_float(c.x << 16), __uint_as_float(c.x & 0xffff0000u),
+                                  __uint_as_float(c.y << 16), __uint_as_float(c.y & 0xffff0000u)};
+            scale(o, old);
+          }
+          uint2 v;
+          v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
+          v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
+          *dst = v;
         }
-        uint2 v;
-        v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
-        v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
-        *dst = v;
       }
     }
   }
@@ -404,7 +424,8 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   GemmParams gp;
   gp.A = static_cast<const uint16_t*>(A);
   gp.B = static_cast<const uint16_t*>(B);
-  gp.C = static_cast<uint16_t*>(C);
+  gp.C = C;
+  gp.c_f32 = p.c_type == DT_FP32 ? 1 : 0;
   gp.a = a;
   gp.b = b;
   gp.c = c;

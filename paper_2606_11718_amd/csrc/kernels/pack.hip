@@ -1,7 +1,8 @@
-// Pack / unpack between row-major (or stored-transpose) bf16 operands and
-// the Chiplet-Contiguous Layout (Sec. III-B, Eq. 3 in block form):
+// Pack / unpack between row-major (or stored-transpose) operands and the
+// Chiplet-Contiguous Layout (Sec. III-B, Eq. 3 in block form); elements of
+// 1, 2 or 4 bytes (fp8, bf16, fp32) are moved as bits:
 //   block b = (r / hr) * Gc + c / wc
-//   elem offset = b * S + (r % hr) * wc + c % wc     (S = padded strip, elements)
+//   byte offset = b * S + ((r % hr) * wc + c % wc) * e     (S = padded strip)
 //
 // The work is enumerated in CCL order: block b, then its q-th element (or
 // 16-byte chunk) in strip order, so every thread's CCL access is the next
@@ -44,16 +45,17 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t q, const DivMagic& m) {
 }
 
 struct PackArgs {
-  const uint16_t* rm;      // row-major side
-  uint16_t* rm_out;        // row-major side when written (unpack)
-  const uint16_t* ccl;     // CCL side (read by unpack)
-  uint16_t* ccl_out;       // CCL side (written by pack)
-  int64_t ld;              // row-major leading dimension, elements
-  int64_t strip;           // padded strip stride, elements
-  int64_t hr, wc;          // block rows / cols
+  const char* rm;          // row-major side
+  char* rm_out;            // row-major side when written (unpack)
+  const char* ccl;         // CCL side (read by unpack)
+  char* ccl_out;           // CCL side (written by pack)
+  int64_t ld_bytes;        // row-major leading dimension
+  int64_t strip;           // padded strip stride, bytes
+  int64_t hr;              // block rows
+  int64_t row_bytes;       // bytes of one block row (wc * e)
   int32_t grid_c;
-  uint32_t units_per_block;  // hr * wc / V
-  DivMagic units_per_row;    // wc / V
+  uint32_t units_per_block;  // hr * row_bytes / sizeof(U)
+  DivMagic units_per_row;    // row_bytes / sizeof(U)
 };
 
 // Load / store one unit; NT = non-temporal (streaming) access.
@@ -68,22 +70,24 @@ __device__ __forceinline__ void st(T* p, T v) {
   else *p = v;
 }
 
-// V = elements per unit (8: one 16-byte vector, 1: one element).
-// UNPACK = false: row-major -> CCL; true: CCL -> row-major.
-// NT: streaming accesses, used for tensors larger than the 256 MiB
-// Infinity Cache (measured: +10 % on a 470 MB copy, -15 % on a 134 MB one).
-template <int V, bool UNPACK, bool NT>
+// U = unit moved per access: one 16-byte vector, or one element (1, 2 or 4
+// bytes) when rows are not 16-byte multiples. UNPACK = false: row-major ->
+// CCL; true: CCL -> row-major. NT: streaming accesses, used for tensors
+// larger than the 256 MiB Infinity Cache (measured: +10 % on a 470 MB copy,
+// -15 % on a 134 MB one).
+template <typename U, bool UNPACK, bool NT>
 __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
   const int32_t b = blockIdx.y;                      // strip / chiplet
   const int64_t pr = b / a.grid_c, pc = b % a.grid_c;
-  const uint16_t* src_rm = a.rm + pr * a.hr * a.ld + pc * a.wc;
-  uint16_t* dst_rm = a.rm_out + pr * a.hr * a.ld + pc * a.wc;
+  const int64_t rm_base = pr * a.hr * a.ld_bytes + pc * a.row_bytes;
+  const char* src_rm = a.rm + rm_base;
+  char* dst_rm = a.rm_out + rm_base;
   const int64_t strip_base = (int64_t)b * a.strip;
   constexpr int UNROLL = 4;
+  constexpr int64_t US = sizeof(U);
   const uint32_t stride = gridDim.x * 256u;
   for (uint32_t base = blockIdx.x * 256u * UNROLL; base < a.units_per_block; base += stride * UNROLL) {
-    using T = typename std::conditional<V == 8, u32x4, uint16_t>::type;
-    T v[UNROLL];
+    U v[UNROLL];
     int64_t rm_off[UNROLL];
     bool ok[UNROLL];
 #pragma unroll
@@ -91,13 +95,13 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       const uint32_t q = base + threadIdx.x + u * 256u;
       ok[u] = q < a.units_per_block;
       const uint32_t row = fdiv(q, a.units_per_row);
-      const uint32_t col = (q - row * a.units_per_row.d) * V;
-      rm_off[u] = (int64_t)row * a.ld + col;
+      const uint32_t col = q - row * a.units_per_row.d;
+      rm_off[u] = (int64_t)row * a.ld_bytes + (int64_t)col * US;
       if (ok[u]) {
         if (UNPACK)
-          v[u] = ld<NT>(reinterpret_cast<const T*>(a.ccl + strip_base + (int64_t)q * V));
+          v[u] = ld<NT>(reinterpret_cast<const U*>(a.ccl + strip_base + (int64_t)q * US));
         else
-          v[u] = ld<NT>(reinterpret_cast<const T*>(src_rm + rm_off[u]));
+          v[u] = ld<NT>(reinterpret_cast<const U*>(src_rm + rm_off[u]));
       }
     }
 #pragma unroll
@@ -105,70 +109,76 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       const uint32_t q = base + threadIdx.x + u * 256u;
       if (ok[u]) {
         if (UNPACK)
-          st<NT>(reinterpret_cast<T*>(dst_rm + rm_off[u]), v[u]);
+          st<NT>(reinterpret_cast<U*>(dst_rm + rm_off[u]), v[u]);
         else
-          st<NT>(reinterpret_cast<T*>(a.ccl_out + strip_base + (int64_t)q * V), v[u]);
+          st<NT>(reinterpret_cast<U*>(a.ccl_out + strip_base + (int64_t)q * US), v[u]);
       }
     }
   }
 }
 
-// Stored-transpose pack: src holds X^T (cols x rows, leading dimension ld),
-// X is rows x cols. A 64 x 64 tile is read along X's rows (contiguous in
-// src), transposed through LDS and written along X's columns (contiguous in
-// the CCL strip). Tiles never straddle blocks (hr, wc multiples of 64).
+// Stored-transpose pack: src holds X^T (cols x rows, leading dimension ld
+// elements), X is rows x cols of element type E. A 64 x 64 tile is read
+// along X's rows (contiguous in src) in 16-byte chunks, transposed through
+// LDS and written in 16-byte chunks along X's columns (contiguous in the
+// CCL strip). Tiles never straddle blocks (hr, wc multiples of 64).
 struct TransArgs {
-  const uint16_t* src;
-  uint16_t* dst;
-  int64_t ld;
-  int64_t strip;
-  int64_t hr, wc;
+  const char* src;
+  char* dst;
+  int64_t ld;              // elements
+  int64_t strip;           // bytes
+  int64_t hr, wc;          // elements
   int32_t grid_c;
-  int32_t tiles_c;         // cols / 64
 };
 
+template <typename E>
 __global__ void __launch_bounds__(256) pack_trans_kernel(TransArgs a) {
-  __shared__ uint16_t tile[64][64 + 8];
+  constexpr int EPC = 16 / sizeof(E);                  // elements per 16-byte chunk
+  constexpr int CPR = 64 / EPC;                        // chunks per 64-element row
+  constexpr int ITER = 64 * CPR / 256;                 // chunks per thread
+  __shared__ E tile[64][64 + 16 / sizeof(E)];
   const int64_t r0 = (int64_t)blockIdx.y * 64;        // X rows = src columns
   const int64_t c0 = (int64_t)blockIdx.x * 64;        // X cols = src rows
   const int t = threadIdx.x;
-  // read: src rows c0..c0+63, 64 elements each = 8 chunks of 16 B
+  const E* src = reinterpret_cast<const E*>(a.src);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < ITER; ++i) {
     const int idx = t + i * 256;
-    const int sr = idx >> 3, ch = idx & 7;
-    uint4 v = *reinterpret_cast<const uint4*>(a.src + (c0 + sr) * a.ld + r0 + ch * 8);
-    const uint16_t* e = reinterpret_cast<const uint16_t*>(&v);
+    const int sr = idx / CPR, ch = idx % CPR;
+    uint4 v = *reinterpret_cast<const uint4*>(src + (c0 + sr) * a.ld + r0 + ch * EPC);
+    const E* e = reinterpret_cast<const E*>(&v);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) tile[sr][ch * 8 + j] = e[j];
+    for (int j = 0; j < EPC; ++j) tile[sr][ch * EPC + j] = e[j];
   }
   __syncthreads();
-  // write: X row r0+xr, columns c0 + 8*ch .. +8, contiguous in the strip
   const int64_t pr = r0 / a.hr, pc = c0 / a.wc;
   const int64_t b = pr * a.grid_c + pc;
-  uint16_t* strip = a.dst + b * a.strip;
+  E* strip = reinterpret_cast<E*>(a.dst + b * a.strip);
   const int64_t rl0 = r0 - pr * a.hr, cl0 = c0 - pc * a.wc;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < ITER; ++i) {
     const int idx = t + i * 256;
-    const int xr = idx >> 3, ch = idx & 7;
+    const int xr = idx / CPR, ch = idx % CPR;
     uint4 v;
-    uint16_t* e = reinterpret_cast<uint16_t*>(&v);
+    E* e = reinterpret_cast<E*>(&v);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) e[j] = tile[ch * 8 + j][xr];
-    *reinterpret_cast<uint4*>(strip + (rl0 + xr) * a.wc + cl0 + ch * 8) = v;
+    for (int j = 0; j < EPC; ++j) e[j] = tile[ch * EPC + j][xr];
+    *reinterpret_cast<uint4*>(strip + (rl0 + xr) * a.wc + cl0 + ch * EPC) = v;
   }
 }
 
 // Any shape: one element per thread, src holds X^T.
+template <typename E>
 __global__ void __launch_bounds__(256) pack_trans_scalar_kernel(TransArgs a, int64_t rows,
                                                                 int64_t cols) {
   const int64_t n = rows * cols;
+  const E* src = reinterpret_cast<const E*>(a.src);
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
     const int64_t r = i / cols, c = i % cols;          // write order: along X rows
     const int64_t pr = r / a.hr, pc = c / a.wc;
     const int64_t b = pr * a.grid_c + pc;
-    a.dst[b * a.strip + (r - pr * a.hr) * a.wc + (c - pc * a.wc)] = a.src[c * a.ld + r];
+    E* strip = reinterpret_cast<E*>(a.dst + b * a.strip);
+    strip[(r - pr * a.hr) * a.wc + (c - pc * a.wc)] = src[c * a.ld + r];
   }
 }
 
@@ -180,65 +190,91 @@ int grid_x_for(uint32_t units, int unroll) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+template <typename U>
+void copy_launch(dim3 grid, const PackArgs& a, bool unpack, hipStream_t stream) {
+  if (unpack)
+    hipLaunchKernelGGL((copy_kernel<U, true, false>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((copy_kernel<U, false, false>), grid, dim3(256), 0, stream, a);
+}
+
+template <typename E>
+void trans_launch(const Layout& L, const TransArgs& a, bool tiled, hipStream_t stream) {
+  if (tiled) {
+    dim3 grid((unsigned)(L.cols / 64), (unsigned)(L.rows / 64));
+    hipLaunchKernelGGL((pack_trans_kernel<E>), grid, dim3(256), 0, stream, a);
+  } else {
+    int64_t n = L.rows * L.cols;
+    int64_t wgs = (n + 255) / 256;
+    if (wgs > 8192) wgs = 8192;
+    hipLaunchKernelGGL((pack_trans_scalar_kernel<E>), dim3((unsigned)wgs), dim3(256), 0, stream, a,
+                       L.rows, L.cols);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, void* ccl_buf,
                        bool unpack, hipStream_t stream) {
   const Layout& L = p.lay[op];
-  const bool vec = (L.block_cols % 8 == 0) && (ld % 8 == 0) && aligned16(rowmajor) &&
+  const int64_t e = L.elem_bytes;
+  const int64_t row_bytes = L.block_cols * e;
+  const bool vec = (row_bytes % 16 == 0) && ((ld * e) % 16 == 0) && aligned16(rowmajor) &&
                    aligned16(ccl_buf) && (L.strip_stride_bytes % 16 == 0);
-  const int V = vec ? 8 : 1;
+  const int64_t unit = vec ? 16 : e;
   PackArgs a;
-  a.rm = static_cast<const uint16_t*>(rowmajor);
-  a.rm_out = const_cast<uint16_t*>(static_cast<const uint16_t*>(rowmajor));
-  a.ccl = static_cast<const uint16_t*>(ccl_buf);
-  a.ccl_out = static_cast<uint16_t*>(ccl_buf);
-  a.ld = ld;
-  a.strip = L.strip_stride_bytes / 2;
+  a.rm = static_cast<const char*>(rowmajor);
+  a.rm_out = const_cast<char*>(static_cast<const char*>(rowmajor));
+  a.ccl = static_cast<const char*>(ccl_buf);
+  a.ccl_out = static_cast<char*>(ccl_buf);
+  a.ld_bytes = ld * e;
+  a.strip = L.strip_stride_bytes;
   a.hr = L.block_rows;
-  a.wc = L.block_cols;
+  a.row_bytes = row_bytes;
   a.grid_c = (int32_t)L.grid_c;
-  a.units_per_block = (uint32_t)(L.block_rows * L.block_cols / V);
-  a.units_per_row = make_div((uint32_t)(L.block_cols / V));
+  a.units_per_block = (uint32_t)(L.block_rows * row_bytes / unit);
+  a.units_per_row = make_div((uint32_t)(row_bytes / unit));
   dim3 grid(grid_x_for(a.units_per_block, 4), (unsigned)(L.grid_r * L.grid_c));
-  const bool nt = L.rows * L.cols * 2 > kInfinityCacheBytes;
-#define CCL_COPY(V_, U_, NT_) hipLaunchKernelGGL((copy_kernel<V_, U_, NT_>), grid, dim3(256), 0, stream, a)
   if (vec) {
-    if (unpack) { if (nt) CCL_COPY(8, true, true); else CCL_COPY(8, true, false); }
-    else        { if (nt) CCL_COPY(8, false, true); else CCL_COPY(8, false, false); }
+    if (L.rows * L.cols * e > kInfinityCacheBytes) {
+      if (unpack)
+        hipLaunchKernelGGL((copy_kernel<u32x4, true, true>), grid, dim3(256), 0, stream, a);
+      else
+        hipLaunchKernelGGL((copy_kernel<u32x4, false, true>), grid, dim3(256), 0, stream, a);
+    } else {
+      copy_launch<u32x4>(grid, a, unpack, stream);
+    }
+  } else if (e == 1) {
+    copy_launch<uint8_t>(grid, a, unpack, stream);
+  } else if (e == 2) {
+    copy_launch<uint16_t>(grid, a, unpack, stream);
   } else {
-    if (unpack) CCL_COPY(1, true, false);
-    else        CCL_COPY(1, false, false);
+    copy_launch<uint32_t>(grid, a, unpack, stream);
   }
-#undef CCL_COPY
   return hipGetLastError();
 }
 
 hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld, void* dst,
                              hipStream_t stream) {
   const Layout& L = p.lay[op];
+  const int64_t e = L.elem_bytes;
   TransArgs a;
-  a.src = static_cast<const uint16_t*>(src);
-  a.dst = static_cast<uint16_t*>(dst);
+  a.src = static_cast<const char*>(src);
+  a.dst = static_cast<char*>(dst);
   a.ld = ld;
-  a.strip = L.strip_stride_bytes / 2;
+  a.strip = L.strip_stride_bytes;
   a.hr = L.block_rows;
   a.wc = L.block_cols;
   a.grid_c = (int32_t)L.grid_c;
-  const bool tiled = L.block_rows % 64 == 0 && L.block_cols % 64 == 0 && ld % 8 == 0 &&
+  const bool tiled = L.block_rows % 64 == 0 && L.block_cols % 64 == 0 && (ld * e) % 16 == 0 &&
                      aligned16(src) && aligned16(dst) && L.strip_stride_bytes % 16 == 0 &&
                      L.rows / 64 <= 65535;
-  if (tiled) {
-    a.tiles_c = (int32_t)(L.cols / 64);
-    dim3 grid((unsigned)(L.cols / 64), (unsigned)(L.rows / 64));
-    hipLaunchKernelGGL(pack_trans_kernel, grid, dim3(256), 0, stream, a);
-  } else {
-    int64_t n = L.rows * L.cols;
-    int64_t wgs = (n + 255) / 256;
-    if (wgs > 8192) wgs = 8192;
-    hipLaunchKernelGGL(pack_trans_scalar_kernel, dim3((unsigned)wgs), dim3(256), 0, stream, a,
-                       L.rows, L.cols);
-  }
+  if (e == 1)
+    trans_launch<uint8_t>(L, a, tiled, stream);
+  else if (e == 2)
+    trans_launch<uint16_t>(L, a, tiled, stream);
+  else
+    trans_launch<uint32_t>(L, a, tiled, stream);
   return hipGetLastError();
 }
 

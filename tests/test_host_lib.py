@@ -200,3 +200,74 @@ def test_ffn_intermediate_needs_no_repack(T, D, F, G, Gr):
     up = ccl.ccl_plan(T, F, D, G, Gr, 4096)
     down = ccl.ccl_plan(T, D, F, G, Gr, 4096)
     assert ccl.ccl_plan_layout(up, ccl.CCL_C) == ccl.ccl_plan_layout(down, ccl.CCL_A)
+
+
+# ---- element types (fp8 E4M3 / bf16 operands, bf16 / fp32 output) ----------
+
+DT = {1: ccl.CCL_DT_FP8_E4M3, 2: ccl.CCL_DT_BF16, 4: ccl.CCL_DT_FP32}
+TYPED = [(1, 2), (1, 4), (2, 4), (2, 2)]          # (e_ab, e_c)
+
+
+@pytest.mark.parametrize("eab,ec", TYPED)
+@pytest.mark.parametrize("M,N,K,Gr,Gc,P,ta,tb", RANDOM_SHAPES[:6])
+def test_typed_layouts_and_remote_bytes_match_oracle(eab, ec, M, N, K, Gr, Gc, P, ta, tb):
+    p = ccl.ccl_plan_typed(M, N, K, Gr * Gc, Gr, P, DT[eab], DT[ec])
+    for op, e in ((ccl.CCL_A, eab), (ccl.CCL_B, eab), (ccl.CCL_C, ec)):
+        lay = ccl.ccl_plan_layout(p, op)
+        R, Cc = OL.operand_shape("ABC"[op], M, N, K)
+        assert lay.elem_bytes == e
+        assert lay.strip_stride_bytes == OL.strip_stride_bytes(R, Cc, Gr, Gc, P, e)
+        assert lay.total_bytes == OL.total_bytes(R, Cc, Gr, Gc, P, e)
+    for name, pl in PLACE.items():
+        got = ccl.ccl_remote_bytes(p, pl, ta | (tb << 1))
+        ref = OT.remote_bytes(M, N, K, Gr, Gc, P, name, ta, tb, e=(eab, eab, ec))
+        for k in ("accessed", "remote", "remote_per_chiplet", "floor", "footprint"):
+            assert got[k] == ref[k], (name, k)
+
+
+@pytest.mark.parametrize("M,N,K,G", [(768, 2048, 4096, 8), (4096, 768, 2048, 8), (8192, 28672, 8192, 8)])
+def test_typed_auto_grid_matches_oracle(M, N, K, G):
+    for eab, ec in TYPED:
+        p = ccl.ccl_plan_typed(M, N, K, G, 0, 4096, DT[eab], DT[ec])
+        assert ccl.ccl_plan_grid(p)[0] == OP.auto_grid_rows(M, N, K, G, e=(eab, eab, ec))
+
+
+def test_typed_plan_rejects_bad_types():
+    for ab, c in ((ccl.CCL_DT_FP32, ccl.CCL_DT_BF16), (ccl.CCL_DT_BF16, ccl.CCL_DT_FP8_E4M3),
+                  (3, 0), (0, -1)):
+        with pytest.raises(ccl.CCLError) as ei:
+            ccl.ccl_plan_typed(256, 512, 256, 4, 2, 4096, ab, c)
+        assert ei.value.status == 1
+
+
+def test_typed_l2_model_matches_oracle():
+    from oracle import l2sim as OL2
+    for eab, ec, ks in ((1, 2, 128), (1, 4, 128), (2, 4, 64)):
+        p = ccl.ccl_plan_typed(256, 512, 512, 4, 2, 4096, DT[eab], DT[ec])
+        for name, pl in PLACE.items():
+            got = ccl.ccl_remote_bytes_l2(p, pl, 1, l2_bytes=8 * 16 * 128, slots=2, k_step=ks)
+            ref = OL2.simulate(256, 512, 512, 2, 2, 4096, name, 1, 0, l2_bytes=8 * 16 * 128, slots=2,
+                               k_step=ks, e=(eab, eab, ec))
+            assert got == ref, (eab, ec, name)
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(256, 512, 256, 4, 2), (4096, 1536, 2048, 8, 2), (768, 2048, 4096, 8, 1),
+                                        (4096, 768, 2048, 8, 8), (8192, 28672, 8192, 8, 2),
+                                        (1024, 768, 1024, 8, 8), (384, 768, 384, 1, 1)])
+@pytest.mark.parametrize("c_type", [ccl.CCL_DT_BF16, ccl.CCL_DT_FP32])
+def test_gemm_host_checks_pass_for_valid_plans(M, N, K, G, Gr, c_type):
+    """Every host-side check of ccl_gemm and ccl_gemm_rowmajor, including the
+    one that every element the kernel can address lies inside the operand
+    buffers, passes for valid plans of either C type: without a GPU the call
+    gets as far as the device query and fails there."""
+    import torch
+    if torch.cuda.device_count() > 0:      # placeholder pointers must never reach a device
+        pytest.skip("needs a host without a GPU")
+    lib = ccl.library()
+    p = ccl.ccl_plan_typed(M, N, K, G, Gr, 4096, ccl.CCL_DT_BF16, c_type)
+    for st in (lib.ccl_gemm(p, 4096, 4096, 4096, None),
+               lib.ccl_gemm_scaled(p, 2.0, 4096, 4096, 1.0, 4096, None),
+               lib.ccl_gemm_rowmajor(p, 4096, 4096, 4096, 0, None)):
+        msg = lib.ccl_last_error().decode()
+        assert "internal" not in msg
+        assert st == 5 and "hipGetDevice" in msg, msg
