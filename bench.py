@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "CCL bf16 GEMM TFLOP/s (% MFMA peak); remote-HBM-byte reduction vs 4KB interleave"
 PEAK_BF16_TFLOPS = 2516.6        # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense)
+PEAK_FP8_TFLOPS = 5033.2         # 256 CU x 8192 FLOP/clk x 2.4 GHz (dense fp8)
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama_fwd_traffic.json")
 GEMM_SRC = os.path.join(ROOT, "paper_2606_11718_amd", "csrc", "kernels", "gemm.hip")
@@ -226,6 +227,42 @@ def remote_report():
     return {"rows": rows, "best_of_grid_geomean_4k": geo}
 
 
+def fp8_gemms(reps: int):
+    """Per-launch time of the fp8 (E4M3) CCL GEMM on the Llama FFN forward
+    shapes (bf16 C), the same kernel structure at twice the MFMA rate per K."""
+    import numpy as np
+    import torch
+    from paper_2606_11718_amd import ccl
+
+    out = {}
+    for name, (M, N, K) in (("llama_up", (8192, 28672, 8192)), ("llama_down", (8192, 8192, 28672))):
+        plan = ccl.ccl_plan_typed(M, N, K, 8, 2, 4096, ccl.CCL_DT_FP8_E4M3, ccl.CCL_DT_BF16)
+        g = torch.Generator(device="cuda").manual_seed(11)
+        A = torch.randn(M * K, device="cuda", generator=g).to(torch.float8_e4m3fn).view(torch.uint8)
+        B = torch.randn(K * N, device="cuda", generator=g).to(torch.float8_e4m3fn).view(torch.uint8)
+        C = torch.empty(M * N, device="cuda", dtype=torch.bfloat16)
+        st = torch.cuda.current_stream()
+        for _ in range(3):
+            ccl.ccl_gemm(plan, A, B, C, st)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+            e0.record(st)
+            ccl.ccl_gemm(plan, A, B, C, st)
+            e1.record(st)
+            ts.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = float(np.mean([a.elapsed_time(b) for a, b in ts]))
+        tf = 2 * M * N * K / ms / 1e9
+        out[name] = {"ms": round(ms, 4), "tflops": round(tf, 1),
+                     "frac_of_fp8_peak": round(tf / PEAK_FP8_TFLOPS, 4)}
+        del A, B, C
+    out["peak"] = PEAK_FP8_TFLOPS
+    out["kernel"] = "gemm_fp8_kernel<256,256,8 waves>, v_mfma_f32_32x32x64_f8f6f4"
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -238,6 +275,7 @@ def main():
     ap.add_argument("--compare-layouts", action="store_true",
                     help="only time CCL vs row-major operands and tile maps, print one JSON line")
     ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--no-fp8", action="store_true", help="skip the fp8 GEMM timing")
     ap.add_argument("--clock-seconds", type=float, default=4.0,
                     help="sustained run after the timed steps that samples clock/power (0: off)")
     args = ap.parse_args()
@@ -387,6 +425,10 @@ def main():
             clk["clock_adjusted_peak_tflops"] = round(PEAK_BF16_TFLOPS * clk["gfx_clock_mhz_median"] / 2400.0, 1)
             clk["gemm_frac_of_clock_adjusted_peak"] = round(achieved / clk["clock_adjusted_peak_tflops"], 4)
         out["sustained_clock"] = clk
+    if not args.no_fp8:
+        del X, Wup_c, Wdn_c, Xc, Hc, Yc, Y
+        torch.cuda.empty_cache()
+        out["fp8_gemm"] = fp8_gemms(args.reps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -103,10 +103,12 @@ bool addressing_in_bounds(const ccl::Plan& p, const ccl::OperandAddr& a, const c
 }
 
 // The kernel addresses a tile's K step with 32-bit byte offsets from its
-// corner: up to 255 rows of A and 31 rows of B.
-bool offsets_fit(const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
+// corner: up to 255 rows of A and one K step minus one rows of B.
+bool offsets_fit(const ccl::Plan& p, const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
   const int64_t lim = ((int64_t)1 << 31) - 4096;
-  return 255 * (int64_t)a.ld * 2 < lim && 31 * (int64_t)b.ld * 2 < lim;
+  const int64_t e = p.lay[ccl::OP_A].elem_bytes;
+  const int64_t bk = p.ab_type == ccl::DT_FP8_E4M3 ? ccl::kGemmBK8 : ccl::kGemmBK;
+  return 255 * (int64_t)a.ld * e < lim && (bk - 1) * (int64_t)b.ld * e < lim;
 }
 
 }  // namespace
@@ -203,7 +205,7 @@ ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, cons
   if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
   ccl::OperandAddr a, b, c;
   ccl_addressing(p, &a, &b, &c);
-  if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
+  if (!offsets_fit(p, a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
   if (!addressing_in_bounds(p, a, b, c, p.lay[ccl::OP_A].total_bytes, p.lay[ccl::OP_B].total_bytes,
                             p.lay[ccl::OP_C].total_bytes))
     return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the CCL buffers");
@@ -228,7 +230,7 @@ ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void
   if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
   ccl::OperandAddr a, b, c;
   rowmajor_addressing(p, &a, &b, &c);
-  if (!offsets_fit(a, b)) return fail(CCL_ERR_UNSUPPORTED, "rows too long for 32-bit in-tile offsets");
+  if (!offsets_fit(p, a, b)) return fail(CCL_ERR_UNSUPPORTED, "rows too long for 32-bit in-tile offsets");
   if (!addressing_in_bounds(p, a, b, c, p.M * p.K * p.lay[ccl::OP_A].elem_bytes,
                             p.K * p.N * p.lay[ccl::OP_B].elem_bytes,
                             p.M * p.N * p.lay[ccl::OP_C].elem_bytes))

@@ -52,12 +52,11 @@ void choose_gemm_config(Plan* p) {
     g.why_unsupported = "chiplets must divide the 8 XCDs";
     return;
   }
-  if (p->ab_type != DT_BF16) {
-    g.why_unsupported = "the GEMM kernels take bf16 A and B";
-    return;
-  }
-  if ((p->K / p->Gc) % kGemmBK != 0 || (p->K / p->Gr) % kGemmBK != 0) {
-    g.why_unsupported = "K / grid_cols and K / grid_rows must be multiples of 32";
+  const int64_t bk = p->ab_type == DT_FP8_E4M3 ? kGemmBK8 : kGemmBK;
+  if ((p->K / p->Gc) % bk != 0 || (p->K / p->Gr) % bk != 0) {
+    g.why_unsupported = p->ab_type == DT_FP8_E4M3
+                            ? "fp8: K / grid_cols and K / grid_rows must be multiples of 64"
+                            : "K / grid_cols and K / grid_rows must be multiples of 32";
     return;
   }
   g.xcd_per_chiplet = kNumXcd / p->G;

@@ -13,7 +13,8 @@ namespace ccl {
 constexpr int kModelTile = 128;   // output tile of the traffic model (Sec. IV-A)
 constexpr int kNumXcd = 8;        // MI355X: 8 XCDs, workgroups dispatched round-robin
 constexpr int kMaxChiplets = 64;
-constexpr int kGemmBK = 32;       // K extent of one GEMM main-loop step
+constexpr int kGemmBK = 32;       // K extent of one GEMM main-loop step (bf16)
+constexpr int kGemmBK8 = 64;      // the same for fp8 operands
 
 enum Op { OP_A = 0, OP_B = 1, OP_C = 2 };
 // Element types (Fig. 7 sweeps the data type): A and B share one type.

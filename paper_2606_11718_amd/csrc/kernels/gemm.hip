@@ -129,6 +129,85 @@ struct FragSet {
   i16x4 b[TN][2];     // two transposed halves (k 0..3 and 4..7) per B fragment
 };
 
+// The output tile (partition pr, pc; tile ti, tj inside it) of this
+// workgroup: the XCD-aware map, or the native grouped raster over the whole
+// tile grid (XCD-oblivious). False when the workgroup has no tile.
+__device__ __forceinline__ bool tile_of_block(const GemmParams& p, int32_t* pr, int32_t* pc,
+                                              int32_t* ti, int32_t* tj) {
+  if (p.remap) return map_tile(p.map, blockIdx.x, pr, pc, ti, tj);
+  const int32_t TMg = p.map.tiles_m * p.grid_r, TNg = p.map.tiles_n * p.map.grid_c;
+  const int32_t t = blockIdx.x;
+  if (t >= TMg * TNg) return false;
+  const int32_t per_group = p.map.group_m * TNg;
+  const int32_t grp = t / per_group, first = grp * p.map.group_m;
+  const int32_t gm = min(p.map.group_m, TMg - first);
+  const int32_t w = t - grp * per_group;
+  const int32_t tig = first + w % gm, tjg = w / gm;
+  *pr = tig / p.map.tiles_m;
+  *ti = tig - *pr * p.map.tiles_m;
+  *pc = tjg / p.map.tiles_n;
+  *tj = tjg - *pc * p.map.tiles_n;
+  return true;
+}
+
+// Epilogue: lane holds C[m][n .. n+3] of each 32x32 MFMA tile (mt, nt) in
+// acc[mt][nt][4q .. 4q+3]; C = alpha * acc (+ beta * C), stored as bf16
+// (nearest even) or fp32.
+template <int BM, int BN, int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&acc)[TM][TN],
+                                           int32_t pr, int32_t pc, int32_t ti, int32_t tj, int wm,
+                                           int wn, int lane) {
+  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  const int epi = p.epi;
+  const float alpha = p.alpha, beta = p.beta;
+  // alpha * acc (+ beta * old) for the four values; old only read when epi == 2.
+  auto scale = [&](float* o, const float* old) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * old[j]) : alpha * o[j];
+  };
+#pragma unroll
+  for (int mt = 0; mt < TM; ++mt) {
+    const int m = wm * WM + mt * 32 + (lane & 31);
+#pragma unroll
+    for (int nt = 0; nt < TN; ++nt) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = wn * WN + nt * 32 + 8 * q + 4 * (lane >> 5);
+        const int64_t idx = c_tile + (int64_t)m * p.c.ld + n;
+        float o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
+        if (p.c_f32) {
+          float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.C) + idx);
+          if (epi != 0) {
+            float old[4] = {0.f, 0.f, 0.f, 0.f};
+            if (epi == 2) {
+              const float4 c = *dst;
+              old[0] = c.x; old[1] = c.y; old[2] = c.z; old[3] = c.w;
+            }
+            scale(o, old);
+          }
+          *dst = make_float4(o[0], o[1], o[2], o[3]);
+        } else {
+          uint2* dst = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.C) + idx);
+          if (epi != 0) {
+            uint2 c = make_uint2(0u, 0u);
+            if (epi == 2) c = *dst;
+            const float old[4] = {__uint_as_float(c.x << 16), __uint_as_float(c.x & 0xffff0000u),
+                                  __uint_as_float(c.y << 16), __uint_as_float(c.y & 0xffff0000u)};
+            scale(o, old);
+          }
+          uint2 v;
+          v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
+          v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
+          *dst = v;
+        }
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int WGN>
 __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) {
   // The host pass only needs the launch stub; the body uses device-only
@@ -148,23 +227,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
 
   int32_t pr, pc, ti, tj;
-  if (p.remap) {
-    if (!map_tile(p.map, blockIdx.x, &pr, &pc, &ti, &tj)) return;
-  } else {
-    // native order: grouped raster over the whole tile grid, XCD-oblivious
-    const int32_t TMg = p.map.tiles_m * p.grid_r, TNg = p.map.tiles_n * p.map.grid_c;
-    const int32_t t = blockIdx.x;
-    if (t >= TMg * TNg) return;
-    const int32_t per_group = p.map.group_m * TNg;
-    const int32_t grp = t / per_group, first = grp * p.map.group_m;
-    const int32_t gm = min(p.map.group_m, TMg - first);
-    const int32_t w = t - grp * per_group;
-    const int32_t tig = first + w % gm, tjg = w / gm;
-    pr = tig / p.map.tiles_m;
-    ti = tig - pr * p.map.tiles_m;
-    pc = tjg / p.map.tiles_n;
-    tj = tjg - pc * p.map.tiles_n;
-  }
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj)) return;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -344,56 +407,255 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     if (s + 3 < ksteps) step(smA3, smB3, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
-  // ---- epilogue: lane holds C[m][n .. n+3] for each (mt, nt, q) ----
-  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
-  const int epi = p.epi;
-  const float alpha = p.alpha, beta = p.beta;
-  // alpha * acc (+ beta * old) for the four values; old only read when epi == 2.
-  auto scale = [&](float* o, const float* old) {
+  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, wm, wn, lane);
+#endif
+}
+
+// ---------------------------------------------------------------------------
+// fp8 (E4M3) operands: C = A B with v_mfma_f32_32x32x64_f8f6f4 (unscaled).
+// A K step is 64 fp8 elements, so one stage holds the same bytes as a bf16
+// step (A rows of 64 bytes, B rows of BN bytes x 64 rows) and the A side
+// (loads, swizzle, fragment reads) is byte-for-byte the bf16 one.
+//
+// Operand pairing of the instruction (probed on gfx950): byte p of lane l in
+// the first operand meets byte p of lanes of the same half (l / 32) in the
+// second, and lane l % 32 selects the row / column. The K index of (half h,
+// byte p) is chosen here as 16h + p for p < 16 and 32 + 16h + (p - 16) for
+// p >= 16: the A fragment is then the two 16-byte chunks h and 2 + h of a
+// 64-byte row, as in the bf16 kernel, and the B fragment is four transposed
+// 8-byte reads (ds_read_b64_tr_b8: within 16 lanes, lane l, byte j comes
+// from source lane 2j + l/8, byte l % 8), each giving 8 consecutive K of one
+// column.
+// ---------------------------------------------------------------------------
+
+constexpr int kBK8 = 64;         // K extent (elements = bytes) of one fp8 step
+
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4v __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
+typedef __attribute__((address_space(3))) i32x4v lds_i32x4;
+
+template <int BM, int BN, int WGN>
+struct Tile8 {
+  static constexpr int NW = 2 * WGN;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr int A_BYTES = BM * kBK8;            // one stage
+  static constexpr int B_BYTES = kBK8 * BN;
+  static constexpr int NA = BM / (16 * NW);            // A: 16 rows of 64 B per load
+  static constexpr int CPR_B = BN / 16;                // 16-byte chunks per B row
+  static constexpr int RPI_B = 64 / CPR_B;             // B rows per load instruction
+  static constexpr int NB = BN / (16 * NW);
+  static constexpr int NL = NA + NB;
+  static_assert(NA >= 1 && NB >= 1 && TN >= 1, "tile too small for the wave grid");
+  static_assert(BN == 128 || BN == 256, "B swizzle is defined for 128- and 256-byte rows");
+};
+
+// B rows (BN bytes): the 8 rows x 2 chunks that 32 lanes of one transposed
+// read touch land in 16 distinct 16-byte bank slots.
+template <int BN>
+__device__ __forceinline__ int swz_b8(int row) {
+  return BN == 256 ? 2 * (row & 7) : (row & 6);
+}
+
+template <int TM, int TN>
+struct FragSet8 {
+  i32x8 a[TM];
+  i32x8 b[TN];
+};
+
+template <int BM, int BN, int WGN>
+__global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using T = Tile8<BM, BN, WGN>;
+  __shared__ __attribute__((aligned(1024))) char smA0[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smA1[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smA2[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smA3[T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB0[T::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB1[T::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB2[T::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
+  static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
+
+  int32_t pr, pc, ti, tj;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj)) return;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const char* A = reinterpret_cast<const char*>(p.A);
+  const char* B = reinterpret_cast<const char*>(p.B);
+
+  // ---- global -> LDS (byte offsets from the K step's tile corner) ----
+  uint32_t a_voff[T::NA];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * old[j]) : alpha * o[j];
-  };
+  for (int i = 0; i < T::NA; ++i) {
+    const int row = 16 * (wave * T::NA + i) + (lane >> 2);
+    const int chunk = (lane & 3) ^ swz_a(row);
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 16);
+  }
+  uint32_t b_voff[T::NB];
 #pragma unroll
-  for (int mt = 0; mt < T::TM; ++mt) {
-    const int m = wm * T::WM + mt * 32 + (lane & 31);
+  for (int i = 0; i < T::NB; ++i) {
+    const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
+    const int chunk = (lane % T::CPR_B) ^ swz_b8<BN>(row);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 16);
+  }
+  const int32_t a_extent = (BM - 1) * p.a.ld + kBK8;
+  const int32_t b_extent = (kBK8 - 1) * p.b.ld + BN;
+
+  // ---- LDS fragment read offsets (bytes) ----
+  int32_t a_rd[2];
+  {
+    const int row = wm * T::WM + (lane & 31);
+    const int h = lane >> 5;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) a_rd[c] = row * 64 + (((2 * c + h) ^ swz_a(row)) * 16);
+  }
+  int32_t b_rd[T::TN][4];
+  {
+    const int g = lane >> 4, s = lane & 15;
+    const int h = g >> 1, cb = g & 1;
 #pragma unroll
     for (int nt = 0; nt < T::TN; ++nt) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = wn * T::WN + nt * 32 + 8 * q + 4 * (lane >> 5);
-        const int64_t idx = c_tile + (int64_t)m * p.c.ld + n;
-        float o[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
-        if (p.c_f32) {
-          float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.C) + idx);
-          if (epi != 0) {
-            float old[4] = {0.f, 0.f, 0.f, 0.f};
-            if (epi == 2) {
-              const float4 c = *dst;
-              old[0] = c.x; old[1] = c.y; old[2] = c.z; old[3] = c.w;
-            }
-            scale(o, old);
-          }
-          *dst = make_float4(o[0], o[1], o[2], o[3]);
-        } else {
-          uint2* dst = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.C) + idx);
-          if (epi != 0) {
-            uint2 c = make_uint2(0u, 0u);
-            if (epi == 2) c = *dst;
-            const float old[4] = {__uint_as_float(c.x << 16), __uint_as_float(c.x & 0xffff0000u),
-                                  __uint_as_float(c.y << 16), __uint_as_float(c.y & 0xffff0000u)};
-            scale(o, old);
-          }
-          uint2 v;
-          v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
-          v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
-          *dst = v;
-        }
+      for (int r = 0; r < 4; ++r) {
+        const int kbase = (r < 2) ? 16 * h + 8 * r : 32 + 16 * h + 8 * (r - 2);
+        const int krow = kbase + (s >> 1);
+        const int col = wn * T::WN + nt * 32 + 16 * cb + 8 * (s & 1);
+        b_rd[nt][r] = krow * BN + (((col >> 4) ^ swz_b8<BN>(krow)) * 16) + (col & 15);
       }
     }
   }
+
+  const char* a_base = A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
+  const char* b_base = B + pc * p.b.part + tj * BN;
+  int64_t a_slice_off = 0, b_slice_off = 0;
+  int32_t a_kl = 0, b_kl = 0;
+
+  struct StageSrc {
+    i32x4 ra, rb;
+  };
+  auto next_src = [&](bool live) {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_base + a_slice_off + a_kl, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_base + b_slice_off + (int64_t)b_kl * p.b.ld, live ? b_extent : 0);
+    a_kl += kBK8;
+    const bool a_wrap = a_kl == p.a.kslice;
+    a_kl = a_wrap ? 0 : a_kl;
+    a_slice_off += a_wrap ? p.a.slice : 0;
+    b_kl += kBK8;
+    const bool b_wrap = b_kl == p.b.kslice;
+    b_kl = b_wrap ? 0 : b_kl;
+    b_slice_off += b_wrap ? p.b.slice : 0;
+    return d;
+  };
+  auto load_one = [&](const StageSrc& d, char* smA, char* smB, int i) {
+    if (i < T::NA)
+      lds_dma16(d.ra, a_voff[i], smA + (wave * T::NA + i) * 1024);
+    else
+      lds_dma16(d.rb, b_voff[i - T::NA], smB + (wave * T::NB + (i - T::NA)) * 1024);
+  };
+  auto load_stage = [&](char* smA, char* smB, bool live) {
+    const StageSrc d = next_src(live);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d, smA, smB, i);
+  };
+
+  using Frags = FragSet8<T::TM, T::TN>;
+  // Reads of one stage's fragments: 2 per A tile (16-byte chunks), 4 per B
+  // tile (8-byte transposed reads), A first.
+  constexpr int kReads = 2 * T::TM + 4 * T::TN;
+  auto read_one = [&](const char* smA, const char* smB, Frags& f, int i) {
+    if (i < 2 * T::TM) {
+      const int mt = i >> 1, c = i & 1;
+      const i32x4v v = *(const lds_i32x4*)(smA + a_rd[c] + mt * 32 * 64);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) f.a[mt][4 * c + j] = v[j];
+    } else {
+      const int nt = (i - 2 * T::TM) >> 2, r = (i - 2 * T::TM) & 3;
+      const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(smB + b_rd[nt][r]));
+      f.b[nt][2 * r] = v[0];
+      f.b[nt][2 * r + 1] = v[1];
+    }
+  };
+  auto read_frags = [&](const char* smA, const char* smB, Frags& f) {
+#pragma unroll
+    for (int i = 0; i < kReads; ++i) read_one(smA, smB, f, i);
+  };
+
+  f32x16 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  constexpr int kMfma = T::TM * T::TN;
+  constexpr int kHalf = (kMfma + 1) / 2;
+  auto mfma_one = [&](const Frags& f, int i) {
+    const int mt = i / T::TN, nt = i % T::TN;
+    acc[mt][nt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(f.b[nt], f.a[mt], acc[mt][nt],
+                                                                  0, 0, 0, 0, 0, 0);
+  };
+  auto stage_barrier = [&]() {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * T::NL, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // One K step on the stage whose fragments are in f: the first half of the
+  // MFMAs issues the loads of the step kStages-1 ahead into (lA, lB); after
+  // the barrier the second half reads the next stage's (nA, nB) fragments
+  // into g. The fragment sets alternate between steps.
+  auto step = [&](const Frags& f, Frags& g, char* lA, char* lB, const char* nA, const char* nB,
+                  bool live) {
+    const StageSrc d = next_src(live);
+#pragma unroll
+    for (int i = 0; i < kHalf; ++i) {
+      mfma_one(f, i);
+      const int per = (T::NL + kHalf - 1) / kHalf;
+#pragma unroll
+      for (int j = 0; j < per; ++j)
+        if (i * per + j < T::NL) load_one(d, lA, lB, i * per + j);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    stage_barrier();
+    constexpr int rest = kMfma - kHalf;
+    constexpr int per = rest > 0 ? (kReads + rest - 1) / rest : kReads;
+#pragma unroll
+    for (int i = 0; i < rest; ++i) {
+      mfma_one(f, kHalf + i);
+#pragma unroll
+      for (int j = 0; j < per; ++j)
+        if (i * per + j < kReads) read_one(nA, nB, g, i * per + j);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (rest == 0) read_frags(nA, nB, g);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  Frags f0, f1;
+  const int32_t ksteps = p.ksteps;
+  load_stage(smA0, smB0, 0 < ksteps);
+  load_stage(smA1, smB1, 1 < ksteps);
+  load_stage(smA2, smB2, 2 < ksteps);
+  stage_barrier();
+  read_frags(smA0, smB0, f0);
+  for (int32_t s = 0; s < ksteps; s += kStages) {
+    step(f0, f1, smA3, smB3, smA1, smB1, s + 3 < ksteps);
+    if (s + 1 < ksteps) step(f1, f0, smA0, smB0, smA2, smB2, s + 4 < ksteps);
+    if (s + 2 < ksteps) step(f0, f1, smA1, smB1, smA3, smB3, s + 5 < ksteps);
+    if (s + 3 < ksteps) step(f1, f0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
+  }
+
+  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, wm, wn, lane);
 #endif
 }
 
@@ -430,7 +692,8 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   gp.b = b;
   gp.c = c;
   gp.map = tile_map(p);
-  gp.ksteps = (int32_t)(p.K / kBK);
+  const bool fp8 = p.ab_type == DT_FP8_E4M3;
+  gp.ksteps = (int32_t)(p.K / (fp8 ? kBK8 : kBK));
   gp.remap = remap ? 1 : 0;
   gp.grid_r = p.Gr;
   gp.alpha = alpha;
@@ -440,6 +703,25 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                              : (unsigned)(g.tiles_m * g.tiles_n * p.G);
   dim3 grid(wgs);
   const int waves = g.waves;
+  if (fp8) {
+#define CCL_LAUNCH8(BM_, BN_, WGN_)                                                    \
+  hipLaunchKernelGGL((gemm_fp8_kernel<BM_, BN_, WGN_>), grid, dim3(Tile8<BM_, BN_, WGN_>::THREADS), \
+                     0, stream, gp)
+    if (g.tile_m == 256 && g.tile_n == 256 && waves == 8)
+      CCL_LAUNCH8(256, 256, 4);
+    else if (g.tile_m == 256 && g.tile_n == 256)
+      CCL_LAUNCH8(256, 256, 2);
+    else if (g.tile_m == 256 && g.tile_n == 128)
+      CCL_LAUNCH8(256, 128, 2);
+    else if (g.tile_m == 128 && g.tile_n == 256)
+      CCL_LAUNCH8(128, 256, 2);
+    else if (g.tile_m == 128 && g.tile_n == 128)
+      CCL_LAUNCH8(128, 128, 2);
+    else
+      return hipErrorInvalidValue;
+#undef CCL_LAUNCH8
+    return hipGetLastError();
+  }
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \
                      stream, gp)
