@@ -160,15 +160,16 @@ ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void
                       int64_t ld, void* stream);
 
 /*
- * C_ccl = A_ccl B_ccl, all three in the plan's CCL layouts: bf16 inputs,
- * fp32 accumulation on the matrix cores, output rounded to nearest even to
- * bf16 or stored as fp32, per the plan's C type (Sec. II-B, III-C). Each XCD computes exactly the output tiles of
+ * C_ccl = A_ccl B_ccl, all three in the plan's CCL layouts: bf16 or fp8
+ * E4M3 inputs (the plan's A/B type), fp32 accumulation on the matrix cores,
+ * output rounded to nearest even to bf16 or stored as fp32, per the plan's C
+ * type (Sec. II-B, III-C; Fig. 7 data types). Each XCD computes exactly the output tiles of
  * the partition its chiplet owns (chiplet c <-> XCDs c*8/G .. c*8/G+8/G-1),
  * so chiplets must divide 8.
  * Errors: CCL_ERR_INVALID_ARG (null pointer); CCL_ERR_MISALIGNED_POINTER
  * (pointer not 16-byte aligned); CCL_ERR_UNSUPPORTED (chiplets not dividing
- * 8, K / Gc or K / Gr not a multiple of 32, A and B not bf16, device not
- * gfx950); CCL_ERR_HIP.
+ * 8, K / Gc or K / Gr not a multiple of 32 for bf16 or of 64 for fp8,
+ * device not gfx950); CCL_ERR_HIP.
  */
 ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
                     void* stream);
