@@ -276,6 +276,8 @@ def main():
                     help="only time CCL vs row-major operands and tile maps, print one JSON line")
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--no-fp8", action="store_true", help="skip the fp8 GEMM timing")
+    ap.add_argument("--fp8-only", action="store_true",
+                    help="only time the fp8 GEMMs, print one JSON line")
     ap.add_argument("--clock-seconds", type=float, default=4.0,
                     help="sustained run after the timed steps that samples clock/power (0: off)")
     args = ap.parse_args()
@@ -296,6 +298,9 @@ def main():
 
     if args.compare_layouts:
         print(json.dumps({"compare_layouts": compare_layouts(args.reps)}), flush=True)
+        return
+    if args.fp8_only:
+        print(json.dumps({"fp8_gemm": fp8_gemms(args.reps)}), flush=True)
         return
 
     dev = torch.device("cuda:0")
