@@ -64,7 +64,7 @@ typedef enum { CCL_A = 0, CCL_B = 1, CCL_C = 2 } ccl_operand;
 typedef enum {
   CCL_DT_BF16 = 0,       /* 2 bytes */
   CCL_DT_FP8_E4M3 = 1,   /* 1 byte: OCP 8-bit float, 4 exponent bits (bias 7), 3 mantissa bits */
-  CCL_DT_FP32 = 2        /* 4 bytes (C only) */
+  CCL_DT_FP32 = 2        /* 4 bytes (C; A and B for layouts and traffic models) */
 } ccl_dtype;
 
 typedef enum {
@@ -118,7 +118,9 @@ ccl_status ccl_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows
 
 /*
  * ccl_plan with element types: ab_type for A and B (CCL_DT_BF16 or
- * CCL_DT_FP8_E4M3), c_type for C (CCL_DT_BF16 or CCL_DT_FP32). The element
+ * CCL_DT_FP8_E4M3; CCL_DT_FP32 is accepted for layouts, pack/unpack and the
+ * traffic models, while ccl_gemm returns CCL_ERR_UNSUPPORTED for it), c_type
+ * for C (CCL_DT_BF16 or CCL_DT_FP32). The element
  * size sets the strip bytes and padding of each layout and the bytes of the
  * traffic models (Sec. II-B: the slice a chiplet needs is N/G elements, so
  * its byte size depends on the type). The automatic grid weighs A and B by

@@ -52,6 +52,10 @@ void choose_gemm_config(Plan* p) {
     g.why_unsupported = "chiplets must divide the 8 XCDs";
     return;
   }
+  if (p->ab_type == DT_FP32) {
+    g.why_unsupported = "the GEMM kernels take bf16 or fp8 A and B (fp32 plans serve layouts and traffic models)";
+    return;
+  }
   const int64_t bk = p->ab_type == DT_FP8_E4M3 ? kGemmBK8 : kGemmBK;
   if ((p->K / p->Gc) % bk != 0 || (p->K / p->Gr) % bk != 0) {
     g.why_unsupported = p->ab_type == DT_FP8_E4M3
@@ -200,8 +204,8 @@ Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, i
     *err = "page_bytes must be a power of two in [128, 2^40]";
     return Status::INVALID_ARG;
   }
-  if ((ab != DT_BF16 && ab != DT_FP8_E4M3) || (c != DT_BF16 && c != DT_FP32)) {
-    *err = "A and B must be bf16 or fp8 E4M3, C bf16 or fp32";
+  if ((ab != DT_BF16 && ab != DT_FP8_E4M3 && ab != DT_FP32) || (c != DT_BF16 && c != DT_FP32)) {
+    *err = "A and B must be bf16, fp8 E4M3 or fp32, C bf16 or fp32";
     return Status::INVALID_ARG;
   }
   const int ea = dtype_bytes(ab), ec = dtype_bytes(c);

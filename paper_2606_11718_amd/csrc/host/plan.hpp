@@ -77,8 +77,8 @@ struct Plan {
 enum class Status { OK = 0, INVALID_ARG = 1, UNALIGNED = 2, UNSUPPORTED = 3, MISALIGNED = 4, HIP = 5 };
 
 // Build a plan. grid_rows == 0 chooses the grid. On error returns the status
-// and fills `err` with a message. ab: type of A and B (bf16 or fp8 E4M3);
-// c: type of C (bf16 or fp32).
+// and fills `err` with a message. ab: type of A and B (bf16, fp8 E4M3, or
+// fp32 for layouts and traffic models only); c: type of C (bf16 or fp32).
 Status make_plan(int64_t M, int64_t N, int64_t K, int chiplets, int grid_rows, int64_t page,
                  DType ab, DType c, Plan* out, std::string* err);
 

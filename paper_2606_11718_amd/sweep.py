@@ -44,15 +44,20 @@ PLACEMENTS = (
     ("coarse", ccl.CCL_PLACE_COARSE, 4096),
     ("ccl", ccl.CCL_PLACE_CCL, 4096),
 )
-K_STEP = 64
 WAYS = 16
 LINE = 128
+ELEM = {ccl.CCL_DT_FP8_E4M3: 1, ccl.CCL_DT_BF16: 2, ccl.CCL_DT_FP32: 4}
+
+
+def k_step(ab_type: int) -> int:
+    """K elements per model step: one 128-byte line of an A row."""
+    return LINE // ELEM[ab_type]
 
 
 def _remote(g, chiplets: int, grid_rows: int, placement: int, page: int, model: str,
-            setting: dict, traversal: int) -> int | None:
+            setting: dict, traversal: int, ab_type: int, c_type: int) -> int | None:
     try:
-        plan = ccl.ccl_plan(g.M, g.N, g.K, chiplets, grid_rows, page)
+        plan = ccl.ccl_plan_typed(g.M, g.N, g.K, chiplets, grid_rows, page, ab_type, c_type)
     except ccl.CCLError as e:
         if e.status == 2:              # grid not tile-aligned for this GEMM
             return None
@@ -62,15 +67,16 @@ def _remote(g, chiplets: int, grid_rows: int, placement: int, page: int, model: 
         return sum(ccl.ccl_remote_bytes(plan, placement, mask)["remote"])
     rec = ccl.ccl_remote_bytes_l2(plan, placement, mask, l2_bytes=setting["l2_bytes"],
                                   slots=setting["slots"], ways=WAYS, line_bytes=LINE,
-                                  k_step=K_STEP, traversal=traversal, threads=1)
+                                  k_step=k_step(ab_type), traversal=traversal, threads=1)
     return sum(rec["remote"])
 
 
 def evaluate(gemms, setting_name="mi300x_like", model: str = "l2", workers: int = 0,
-             log=None) -> list[dict]:
+             log=None, ab_type: int = ccl.CCL_DT_BF16, c_type: int = ccl.CCL_DT_BF16) -> list[dict]:
     """Best (grid, traversal) remote bytes of every GEMM under every placement.
 
     setting_name: a key of SETTINGS, or a dict with the same fields.
+    ab_type / c_type: element types of A, B and of C (Fig. 7 data types).
     """
     setting = SETTINGS[setting_name] if isinstance(setting_name, str) else dict(setting_name)
     if not isinstance(setting_name, str):
@@ -85,7 +91,7 @@ def evaluate(gemms, setting_name="mi300x_like", model: str = "l2", workers: int 
     def run(job):
         gi, name, gr, tr = job
         pl, page = place[name]
-        return job, _remote(gemms[gi], G, gr, pl, page, model, setting, tr)
+        return job, _remote(gemms[gi], G, gr, pl, page, model, setting, tr, ab_type, c_type)
 
     best: dict = {}
     workers = workers or max(1, os.cpu_count() or 1)
@@ -105,7 +111,8 @@ def evaluate(gemms, setting_name="mi300x_like", model: str = "l2", workers: int 
     for gi, g in enumerate(gemms):
         rec = {"gemm": g.name, "model": g.model, "tokens": g.tokens, "proj": g.proj, "pass": g.pass_,
                "M": g.M, "N": g.N, "K": g.K, "trans_a": g.a_trans, "trans_b": g.b_trans,
-               "setting": setting_name, "traffic_model": model}
+               "setting": setting_name, "traffic_model": model,
+               "elem_bytes": [ELEM[ab_type], ELEM[ab_type], ELEM[c_type]]}
         if (gi, "ccl") not in best:        # no tile-aligned grid for this GEMM
             rec["no_aligned_grid"] = True
             out.append(rec)
@@ -143,6 +150,34 @@ def summarize(records: list[dict]) -> dict:
     return out
 
 
+def fig7(workers: int = 0, log=None) -> dict:
+    """The sensitivity study of Fig. 7 in the finite-L2 model: mean remote
+    bytes over the 12 GEMMs with 4K tokens (each placement at its best grid
+    and traversal) while the per-chiplet L2 capacity varies with bf16
+    operands, and while the data type varies with an 8 MB L2. Chiplets and
+    resident tiles as in the MI300X-like setting."""
+    import workloads as W
+
+    gemms = [g for g in W.FFN_SWEEP if g.tokens == 4096]
+    base = dict(SETTINGS["mi300x_like"])
+    names = ("rr_4k", "coarse", "ccl")
+
+    def mean_remote(setting, ab, c):
+        recs = evaluate(gemms, setting, "l2", workers, log, ab, c)
+        recs = [r for r in recs if not r.get("no_aligned_grid")]
+        return {n: sum(r[n]["remote_bytes"] for r in recs) / len(recs) for n in names}
+
+    out = {"gemms": len(gemms), "capacity_sweep_bf16": {}, "dtype_sweep_8mb": {}}
+    for mb in (2, 4, 8, 16, 32):
+        st = dict(base, l2_bytes=mb * MIB)
+        out["capacity_sweep_bf16"][f"{mb}MB"] = mean_remote(st, ccl.CCL_DT_BF16, ccl.CCL_DT_BF16)
+    for label, ab, c in (("fp8 (bf16 C)", ccl.CCL_DT_FP8_E4M3, ccl.CCL_DT_BF16),
+                         ("bf16", ccl.CCL_DT_BF16, ccl.CCL_DT_BF16),
+                         ("fp32", ccl.CCL_DT_FP32, ccl.CCL_DT_FP32)):
+        out["dtype_sweep_8mb"][label] = mean_remote(dict(base, l2_bytes=8 * MIB), ab, c)
+    return out
+
+
 def markdown(records: list[dict]) -> str:
     cols = [name for name, _, _ in PLACEMENTS]
     lines = ["| GEMM | M×N×K | " + " | ".join(cols) + " | CCL grid | class |",
@@ -172,7 +207,16 @@ def main(argv=None) -> int:
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--out", default="", help="write the records and summary as JSON here")
     ap.add_argument("--markdown", action="store_true", help="print a markdown table")
+    ap.add_argument("--fig7", action="store_true",
+                    help="L2-capacity and data-type sensitivity (mean over the 4K-token GEMMs)")
     a = ap.parse_args(argv)
+    if a.fig7:
+        res = fig7(a.workers, log=lambda m: print(m, file=sys.stderr))
+        if a.out:
+            with open(a.out, "w") as f:
+                json.dump(res, f, indent=1)
+        print(json.dumps(res, indent=1))
+        return 0
     gemms = list(W.FFN_SWEEP)
     if a.models:
         gemms = [g for g in gemms if g.model in a.models.split(",")]

@@ -205,7 +205,7 @@ def test_ffn_intermediate_needs_no_repack(T, D, F, G, Gr):
 # ---- element types (fp8 E4M3 / bf16 operands, bf16 / fp32 output) ----------
 
 DT = {1: ccl.CCL_DT_FP8_E4M3, 2: ccl.CCL_DT_BF16, 4: ccl.CCL_DT_FP32}
-TYPED = [(1, 2), (1, 4), (2, 4), (2, 2)]          # (e_ab, e_c)
+TYPED = [(1, 2), (1, 4), (2, 4), (2, 2), (4, 4)]  # (e_ab, e_c)
 
 
 @pytest.mark.parametrize("eab,ec", TYPED)
@@ -233,7 +233,7 @@ def test_typed_auto_grid_matches_oracle(M, N, K, G):
 
 
 def test_typed_plan_rejects_bad_types():
-    for ab, c in ((ccl.CCL_DT_FP32, ccl.CCL_DT_BF16), (ccl.CCL_DT_BF16, ccl.CCL_DT_FP8_E4M3),
+    for ab, c in ((ccl.CCL_DT_BF16, ccl.CCL_DT_FP8_E4M3), (ccl.CCL_DT_FP8_E4M3, ccl.CCL_DT_FP8_E4M3),
                   (3, 0), (0, -1)):
         with pytest.raises(ccl.CCLError) as ei:
             ccl.ccl_plan_typed(256, 512, 256, 4, 2, 4096, ab, c)
@@ -271,3 +271,11 @@ def test_gemm_host_checks_pass_for_valid_plans(M, N, K, G, Gr, c_type):
         msg = lib.ccl_last_error().decode()
         assert "internal" not in msg
         assert st == 5 and "hipGetDevice" in msg, msg
+
+
+def test_fp32_operand_plan_has_no_gemm():
+    p = ccl.ccl_plan_typed(256, 512, 256, 4, 2, 4096, ccl.CCL_DT_FP32, ccl.CCL_DT_FP32)
+    assert ccl.ccl_plan_layout(p, ccl.CCL_A).elem_bytes == 4
+    lib = ccl.library()
+    assert lib.ccl_gemm(p, 4096, 4096, 4096, None) == 3      # unsupported, before any device call
+    assert "bf16 or fp8" in lib.ccl_last_error().decode()

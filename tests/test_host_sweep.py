@@ -46,7 +46,7 @@ def _toy():
     return out
 
 
-def _oracle_best(g, G, model, setting):
+def _oracle_best(g, G, model, setting, e=(2, 2, 2)):
     best = {}
     for name, (pl, page) in PLACE_ORACLE.items():
         for gr in range(1, G + 1):
@@ -55,12 +55,12 @@ def _oracle_best(g, G, model, setting):
             for trav in (("row", "col") if model == "l2" else ("row",)):
                 if model == "charge":
                     rb = OT.total_remote(OT.remote_bytes(g.M, g.N, g.K, gr, G // gr, page, pl,
-                                                         g.a_trans, g.b_trans))
+                                                         g.a_trans, g.b_trans, e=e))
                 else:
                     rb = OL2.total_remote(OL2.simulate(
                         g.M, g.N, g.K, gr, G // gr, page, pl, g.a_trans, g.b_trans,
                         l2_bytes=setting["l2_bytes"], slots=setting["slots"], ways=sweep.WAYS,
-                        line=sweep.LINE, k_step=sweep.K_STEP, traversal=trav))
+                        line=sweep.LINE, k_step=sweep.LINE // e[0], traversal=trav, e=e))
                 if name not in best or rb < best[name]:
                     best[name] = rb
     return best
@@ -76,6 +76,19 @@ def test_best_configuration_matches_oracle(model):
         for name in PLACE_ORACLE:
             assert r[name]["remote_bytes"] == want[name], (g.name, name)
         assert r["coarse_optimal"] == (want["coarse"] <= want["ccl"])
+
+
+@pytest.mark.parametrize("ab,c,e", [(1, 0, (1, 1, 2)), (2, 2, (4, 4, 4))])
+def test_typed_best_configuration_matches_oracle(ab, c, e):
+    """fp8 operands with a bf16 C, and fp32 throughout (Fig. 7 data types)."""
+    setting = dict(chiplets=4, l2_bytes=64 * 1024, slots=3)
+    gemms = _toy()[:6]
+    recs = sweep.evaluate(gemms, setting, "l2", workers=4, ab_type=ab, c_type=c)
+    for g, r in zip(gemms, recs):
+        want = _oracle_best(g, 4, "l2", setting, e)
+        for name in PLACE_ORACLE:
+            assert r[name]["remote_bytes"] == want[name], (g.name, name)
+        assert r["elem_bytes"] == list(e)
 
 
 def test_gemm_without_aligned_grid_is_reported():
