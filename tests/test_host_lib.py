@@ -279,3 +279,17 @@ def test_fp32_operand_plan_has_no_gemm():
     lib = ccl.library()
     assert lib.ccl_gemm(p, 4096, 4096, 4096, None) == 3      # unsupported, before any device call
     assert "bf16 or fp8" in lib.ccl_last_error().decode()
+
+
+def test_size_limits_are_rejected_before_any_launch():
+    """Shapes past the kernels' 32-bit in-tile byte offsets, or with a CCL
+    strip of 2^31 elements or more, are refused on the host (status
+    CCL_ERR_UNSUPPORTED) before any device call."""
+    lib = ccl.library()
+    wide = ccl.ccl_plan(256, 128, 1 << 23, 1, 1, 4096)      # 255 rows of A span > 2^31 bytes
+    assert lib.ccl_gemm(wide, 4096, 4096, 4096, None) == 3
+    assert "32-bit" in lib.ccl_last_error().decode()
+    assert lib.ccl_gemm_rowmajor(wide, 4096, 4096, 4096, 1, None) == 3
+    huge = ccl.ccl_plan(65536, 128, 65536, 1, 1, 4096)      # one strip of 2^32 elements
+    assert lib.ccl_pack(huge, ccl.CCL_A, 4096, 65536, 0, 4096, None) == 3
+    assert lib.ccl_unpack(huge, ccl.CCL_A, 4096, 4096, 65536, None) == 3
