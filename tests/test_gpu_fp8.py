@@ -162,3 +162,26 @@ def test_fp8_llama_forward_sampled(name):
     err = OG.errors(got.astype(np.float64), ref)
     print(name, "sampled errors", err, flush=True)
     assert err["rel_fro"] <= 1e-4
+
+
+@pytest.mark.parametrize("remap", [0, 1])
+@pytest.mark.parametrize("c_type", [ccl.CCL_DT_BF16, ccl.CCL_DT_FP32])
+def test_fp8_rowmajor_baseline(remap, c_type):
+    """The same fp8 kernel on plain row-major operands (the layout the paper
+    starts from), with the native or the XCD-aware tile map."""
+    M, N, K, G, Gr = 1024, 2048, 1024, 8, 2
+    A = W.draw_array_fp8(97, M, K, "normal", 1.0)
+    B = W.draw_array_fp8(98, K, N, "normal", 1.0)
+    plan = ccl.ccl_plan_typed(M, N, K, G, Gr, 4096, ccl.CCL_DT_FP8_E4M3, c_type)
+    e = 4 if c_type == ccl.CCL_DT_FP32 else 2
+    print(f"fp8 rowmajor {M}x{N}x{K} remap={remap} c_bytes={e}", flush=True)
+    Cd = _dev_bytes(M * N * e)
+    ccl.ccl_gemm_rowmajor(plan, _to_dev(A), _to_dev(B), Cd, remap)
+    Cb = _from_dev(Cd, np.uint32 if e == 4 else np.uint16).reshape(M, N)
+    C = Cb.view(np.float32).astype(np.float64) if e == 4 else OG.decode_bf16(Cb)
+    err = OG.errors(C, OG.gemm_fp64(A, B))
+    print("errors", err, flush=True)
+    if e == 4:
+        assert err["rel_fro"] <= 1e-4
+    else:
+        assert OG.within_tolerance(err)
