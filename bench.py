@@ -263,6 +263,44 @@ def fp8_gemms(reps: int):
     return out
 
 
+def workload_gemms(reps: int):
+    """Per-launch time of ccl_gemm on every workload GEMM shape (bf16, random
+    operands already in CCL), at the grid the parity tests use: the small
+    Qwen3 shapes, the tiny case and the Llama backward GEMMs."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2606_11718_amd import ccl
+
+    out = {}
+    for wl in W.WORKLOADS.values():
+        for g in wl.gemms:
+            gr_req = g.grids[0]
+            plan = ccl.ccl_plan(g.M, g.N, g.K, g.chiplets, gr_req, 4096)
+            gr, gc = ccl.ccl_plan_grid(plan)
+            lay = [ccl.ccl_plan_layout(plan, op) for op in (ccl.CCL_A, ccl.CCL_B, ccl.CCL_C)]
+            gen = torch.Generator(device="cuda").manual_seed(5)
+            A = torch.randn(lay[0].total_bytes // 2, device="cuda", generator=gen).to(torch.bfloat16)
+            B = (torch.randn(lay[1].total_bytes // 2, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+            C = torch.empty(lay[2].total_bytes // 2, device="cuda", dtype=torch.bfloat16)
+            st = torch.cuda.current_stream()
+            for _ in range(3):
+                ccl.ccl_gemm(plan, A, B, C, st)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+            e0.record(st)
+            for _ in range(reps):
+                ccl.ccl_gemm(plan, A, B, C, st)
+            e1.record(st)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            tm, tn, _ = ccl.ccl_debug_gemm_config(plan)
+            out[g.name] = {"MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
+                           "ms": round(ms, 4), "tflops": round(g.flops / ms / 1e9, 1)}
+            del A, B, C
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -278,6 +316,8 @@ def main():
     ap.add_argument("--no-fp8", action="store_true", help="skip the fp8 GEMM timing")
     ap.add_argument("--fp8-only", action="store_true",
                     help="only time the fp8 GEMMs, print one JSON line")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip timing the GEMM of every workload shape")
     ap.add_argument("--clock-seconds", type=float, default=4.0,
                     help="sustained run after the timed steps that samples clock/power (0: off)")
     args = ap.parse_args()
@@ -430,10 +470,12 @@ def main():
             clk["clock_adjusted_peak_tflops"] = round(PEAK_BF16_TFLOPS * clk["gfx_clock_mhz_median"] / 2400.0, 1)
             clk["gemm_frac_of_clock_adjusted_peak"] = round(achieved / clk["clock_adjusted_peak_tflops"], 4)
         out["sustained_clock"] = clk
+    del X, Wup_c, Wdn_c, Xc, Hc, Yc, Y
+    torch.cuda.empty_cache()
     if not args.no_fp8:
-        del X, Wup_c, Wdn_c, Xc, Hc, Yc, Y
-        torch.cuda.empty_cache()
         out["fp8_gemm"] = fp8_gemms(args.reps)
+    if not args.no_workloads:
+        out["workload_gemms"] = workload_gemms(args.reps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(out), flush=True)
