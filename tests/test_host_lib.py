@@ -293,3 +293,16 @@ def test_size_limits_are_rejected_before_any_launch():
     huge = ccl.ccl_plan(65536, 128, 65536, 1, 1, 4096)      # one strip of 2^32 elements
     assert lib.ccl_pack(huge, ccl.CCL_A, 4096, 65536, 0, 4096, None) == 3
     assert lib.ccl_unpack(huge, ccl.CCL_A, 4096, 4096, 65536, None) == 3
+
+
+def test_one_plan_from_many_host_threads():
+    """A plan is immutable: concurrent host calls on it give the serial results."""
+    from concurrent.futures import ThreadPoolExecutor
+    p = ccl.ccl_plan(4096, 1536, 2048, 8, 2, 4096)
+    want = [ccl.ccl_remote_bytes(p, pl, m) for pl in range(3) for m in range(8)]
+    def job(i):
+        pl, m = divmod(i % 24, 8)
+        return i % 24, ccl.ccl_remote_bytes(p, pl, m)
+    with ThreadPoolExecutor(max_workers=8) as ex:
+        for i, got in ex.map(job, range(96)):
+            assert got == want[i]
