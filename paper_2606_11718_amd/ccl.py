@@ -23,8 +23,9 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
                 3: "CCL_ERR_UNSUPPORTED", 4: "CCL_ERR_MISALIGNED_POINTER", 5: "CCL_ERR_HIP"}
 
 # every symbol include/ccl.h declares
-EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout", "ccl_pack",
-            "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
+EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout",
+            "ccl_pack", "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_rowmajor",
+            "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
