@@ -28,6 +28,10 @@
  *     host-only and need no GPU.
  *   - Every call returns a ccl_status. On any error nothing is written and
  *     nothing is launched; ccl_last_error() gives a per-thread message.
+ *   - Tuning overrides, read when a plan is made: CCL_GEMM_TILE=RxC (kernel
+ *     tile 256x256, 256x128, 128x256 or 128x128), CCL_GEMM_WAVES=4|8 (waves
+ *     of a 256x256 tile) and CCL_GEMM_GROUP_M=n (rows of the tile raster
+ *     group). Unset, the plan chooses.
  *
  * CCL layout of an operand X (R x Cc) under a Gr x Gc grid (the same grid
  * is laid over each operand's own rows and columns: A is split along K by
@@ -228,7 +232,9 @@ typedef struct {
   int32_t slots;      /* tiles a chiplet runs at once (its CTA concurrency), >= 1 */
   int32_t k_step;     /* K elements every resident tile reads per step, >= 1 */
   int32_t traversal;  /* order of a chiplet's tiles: 0 tile rows outer, 1 tile columns outer */
-  int32_t threads;    /* host threads; 0 = one per chiplet, up to the core count */
+  int32_t threads;    /* host threads (capped at the core count); 0 = one per chiplet,
+                         up to the core count. Each thread holds one chiplet's tags:
+                         l2_bytes / line_bytes * 8 bytes of host memory. */
 } ccl_l2_config;
 
 /* Result of ccl_remote_bytes_l2. Index [0]=A, [1]=B, [2]=C. */

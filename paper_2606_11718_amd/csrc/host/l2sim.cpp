@@ -245,8 +245,10 @@ L2Traffic remote_bytes_l2(const Plan& p, Placement pl, int flags, const L2Config
                   make_stored(p, OP_B, pl, (trans_mask >> 1) & 1, c.line),
                   make_stored(p, OP_C, pl, false, c.line)};
   std::vector<ChipletCount> per(p.G);
-  int nthreads = c.threads;
-  if (nthreads == 0) nthreads = std::max(1u, std::thread::hardware_concurrency());
+  // Each thread holds one chiplet's tag array (l2_bytes / line * 8 bytes), so
+  // never run more threads than there are cores.
+  const int cores = static_cast<int>(std::max(1u, std::thread::hardware_concurrency()));
+  int nthreads = c.threads == 0 ? cores : std::min(c.threads, cores);
   nthreads = std::min(nthreads, p.G);
   std::atomic<int> next{0};
   auto worker = [&] {
