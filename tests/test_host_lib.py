@@ -306,3 +306,26 @@ def test_one_plan_from_many_host_threads():
     with ThreadPoolExecutor(max_workers=8) as ex:
         for i, got in ex.map(job, range(96)):
             assert got == want[i]
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr,why", [
+    (384, 768, 384, 3, 1, "divide the 8"),           # 3 chiplets do not map onto 8 XCDs
+    (2048, 1024, 256, 16, 2, "divide the 8"),        # more chiplets than XCDs
+    (256, 512, 48, 2, 1, "multiples of 32"),         # K / Gc = 24 is not a whole K step
+    (256, 512, 96, 1, 1, "multiples of 32"),
+])
+def test_gemm_unsupported_plans_are_refused_on_the_host(M, N, K, G, Gr, why):
+    """Valid plans (layouts and traffic models work) whose GEMM the kernels
+    cannot run: ccl_gemm says so before any device call."""
+    p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+    assert ccl.ccl_plan_layout(p, ccl.CCL_A).total_bytes > 0
+    lib = ccl.library()
+    assert lib.ccl_gemm(p, 4096, 4096, 4096, None) == 3
+    assert why in lib.ccl_last_error().decode()
+
+
+def test_fp8_gemm_needs_64_element_k_steps():
+    p = ccl.ccl_plan_typed(256, 512, 96, 1, 1, 4096, ccl.CCL_DT_FP8_E4M3, ccl.CCL_DT_BF16)
+    lib = ccl.library()
+    assert lib.ccl_gemm(p, 4096, 4096, 4096, None) == 3
+    assert "64" in lib.ccl_last_error().decode()
