@@ -312,7 +312,7 @@ def test_one_plan_from_many_host_threads():
     (384, 768, 384, 3, 1, "divide the 8"),           # 3 chiplets do not map onto 8 XCDs
     (2048, 1024, 256, 16, 2, "divide the 8"),        # more chiplets than XCDs
     (256, 512, 48, 2, 1, "multiples of 32"),         # K / Gc = 24 is not a whole K step
-    (256, 512, 96, 1, 1, "multiples of 32"),
+    (256, 512, 80, 1, 1, "multiples of 32"),         # K = 80: two and a half K steps
 ])
 def test_gemm_unsupported_plans_are_refused_on_the_host(M, N, K, G, Gr, why):
     """Valid plans (layouts and traffic models work) whose GEMM the kernels
