@@ -284,19 +284,32 @@ def workload_gemms(reps: int):
             B = (torch.randn(lay[1].total_bytes // 2, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
             C = torch.empty(lay[2].total_bytes // 2, device="cuda", dtype=torch.bfloat16)
             st = torch.cuda.current_stream()
-            for _ in range(3):
-                ccl.ccl_gemm(plan, A, B, C, st)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
-            e0.record(st)
-            for _ in range(reps):
-                ccl.ccl_gemm(plan, A, B, C, st)
-            e1.record(st)
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1) / reps
+
+            def timed(call):
+                for _ in range(3):
+                    call()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+                e0.record(st)
+                for _ in range(reps):
+                    call()
+                e1.record(st)
+                torch.cuda.synchronize()
+                return e0.elapsed_time(e1) / reps
+
+            ms = timed(lambda: ccl.ccl_gemm(plan, A, B, C, st))
             tm, tn, _ = ccl.ccl_debug_gemm_config(plan)
-            out[g.name] = {"MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
-                           "ms": round(ms, 4), "tflops": round(g.flops / ms / 1e9, 1)}
+            rec = {"MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
+                   "ms": round(ms, 4), "tflops": round(g.flops / ms / 1e9, 1)}
+            ranges, ws_bytes = ccl.ccl_gemm_splitk_workspace(plan, 0)
+            if ranges > 1:             # the library's split-K choice for this shape
+                ws = torch.empty(ws_bytes, device="cuda", dtype=torch.uint8)
+                ms_s = timed(lambda: ccl.ccl_gemm_splitk(plan, 1.0, A, B, 0.0, C, ranges, ws,
+                                                         ws_bytes, st))
+                rec["splitk"] = {"ranges": ranges, "ms": round(ms_s, 4),
+                                 "tflops": round(g.flops / ms_s / 1e9, 1)}
+                del ws
+            out[g.name] = rec
             del A, B, C
     return out
 

@@ -193,6 +193,43 @@ ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, cons
                            float beta, void* C_ccl, void* stream);
 
 /*
+ * Split-K form of ccl_gemm_scaled, for GEMMs whose partitions have fewer
+ * output tiles than an XCD has compute units (small M x N, long K: e.g. the
+ * weight gradients of Sec. IV-A). Not a method of the paper: the ownership of
+ * Sec. II-B is kept, as every K range of a tile, its fp32 partial and the
+ * reduction that writes the tile all run on XCDs of the chiplet owning it.
+ *
+ * ccl_gemm_splitk_workspace: in: *splits = the requested number of K
+ * ranges per tile (1..16), or 0 to let the library choose (enough ranges to
+ * give each of an XCD's 32 compute units a workgroup, each range at least 8
+ * main-loop steps). out: *splits = the number of non-empty ranges actually
+ * used (the K steps, 32 bf16 or 64 fp8 elements each, are cut into ranges
+ * of ceil(steps / requested)), *workspace_bytes = the device workspace that
+ * ccl_gemm_splitk needs for that request: G * tiles * ranges * tile_m *
+ * tile_n * 4 bytes, 0 when one range is used.
+ *
+ * ccl_gemm_splitk: C_ccl = alpha * A_ccl B_ccl + beta * C_ccl as
+ * ccl_gemm_scaled, with `splits` as requested above. With more than one
+ * range, two kernels run in order on `stream`: the K ranges write fp32
+ * partial tiles to `workspace` (caller-owned device memory, 16-byte
+ * aligned, at least the size reported for the same plan and splits; its
+ * contents on entry do not matter and are left undefined), then each tile's
+ * partials are summed in ascending range order in fp32 and alpha * sum +
+ * beta * c is stored in C's type. One range: exactly ccl_gemm_scaled, and
+ * the workspace is not used (may be NULL). Calls that share a workspace
+ * must be ordered on one stream.
+ * Errors: as ccl_gemm_scaled; CCL_ERR_INVALID_ARG also for NULL splits or
+ * workspace_bytes, splits outside 0..16 (workspace query) or 1..16 (GEMM),
+ * or a NULL or too small workspace when more than one range is used;
+ * CCL_ERR_MISALIGNED_POINTER for a workspace not 16-byte aligned;
+ * CCL_ERR_UNSUPPORTED when the split grid would exceed 2^31 workgroups.
+ */
+ccl_status ccl_gemm_splitk_workspace(ccl_plan_t plan, int* splits, int64_t* workspace_bytes);
+ccl_status ccl_gemm_splitk(ccl_plan_t plan, float alpha, const void* A_ccl, const void* B_ccl,
+                           float beta, void* C_ccl, int splits, void* workspace,
+                           int64_t workspace_bytes, void* stream);
+
+/*
  * Baseline for comparison with ccl_gemm (the layout the paper starts from,
  * Sec. II-B Eq. 2): the same GEMM kernel on plain row-major operands
  * A (M x K), B (K x N) and C (M x N), leading dimensions K, N and N, with

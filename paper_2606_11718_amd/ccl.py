@@ -24,8 +24,8 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 
 # every symbol include/ccl.h declares
 EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout",
-            "ccl_pack", "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_rowmajor",
-            "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
+            "ccl_pack", "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_splitk_workspace",
+            "ccl_gemm_splitk", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
@@ -88,6 +88,8 @@ def library() -> ctypes.CDLL:
         "ccl_unpack": [vp, i32, vp, vp, i64, vp],
         "ccl_gemm": [vp, vp, vp, vp, vp],
         "ccl_gemm_scaled": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, vp],
+        "ccl_gemm_splitk_workspace": [vp, ctypes.POINTER(i32), ctypes.POINTER(i64)],
+        "ccl_gemm_splitk": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, i32, vp, i64, vp],
         "ccl_gemm_rowmajor": [vp, vp, vp, vp, i32, vp],
         "ccl_remote_bytes": [vp, i32, i32, ctypes.POINTER(_Traffic)],
         "ccl_remote_bytes_l2": [vp, i32, i32, ctypes.POINTER(_L2Config), ctypes.POINTER(_L2Traffic)],
@@ -207,6 +209,20 @@ def ccl_gemm(plan: Plan, A_ccl, B_ccl, C_ccl, stream=None) -> None:
 def ccl_gemm_scaled(plan: Plan, alpha: float, A_ccl, B_ccl, beta: float, C_ccl, stream=None) -> None:
     _check(library().ccl_gemm_scaled(plan, alpha, _ptr(A_ccl), _ptr(B_ccl), beta, _ptr(C_ccl),
                                      _stream(stream)))
+
+
+def ccl_gemm_splitk_workspace(plan: Plan, splits: int = 0) -> tuple[int, int]:
+    """(K ranges used, workspace bytes) for a requested split count (0: choose)."""
+    s = ctypes.c_int(splits)
+    nbytes = ctypes.c_int64(0)
+    _check(library().ccl_gemm_splitk_workspace(plan, ctypes.byref(s), ctypes.byref(nbytes)))
+    return s.value, nbytes.value
+
+
+def ccl_gemm_splitk(plan: Plan, alpha: float, A_ccl, B_ccl, beta: float, C_ccl, splits: int,
+                    workspace, workspace_bytes: int, stream=None) -> None:
+    _check(library().ccl_gemm_splitk(plan, alpha, _ptr(A_ccl), _ptr(B_ccl), beta, _ptr(C_ccl),
+                                     splits, _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
 def ccl_gemm_rowmajor(plan: Plan, A, B, C, remap: int, stream=None) -> None:

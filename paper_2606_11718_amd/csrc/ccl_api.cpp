@@ -210,9 +210,59 @@ ccl_status ccl_gemm_scaled(ccl_plan_t plan, float alpha, const void* A_ccl, cons
                             p.lay[ccl::OP_C].total_bytes))
     return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the CCL buffers");
   if (ccl_status s = check_device()) return s;
-  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, alpha, beta,
-                                     static_cast<hipStream_t>(stream)),
+  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, alpha, beta, 1,
+                                     nullptr, static_cast<hipStream_t>(stream)),
                     "gemm launch");
+}
+
+// The split-K launch has about splits times the workgroups of the plain
+// GEMM, its reduce launch tile_m * tile_n / 1024 times as many.
+static ccl_status check_split_grid(const ccl::Plan& p, int splits) {
+  if (ccl::splitk_workgroups(p, splits) > 0x7fffffff ||
+      ccl::splitk_reduce_workgroups(p) > 0x7fffffff)
+    return fail(CCL_ERR_UNSUPPORTED, "split-K grid exceeds the launch limit");
+  return ok();
+}
+
+ccl_status ccl_gemm_splitk_workspace(ccl_plan_t plan, int* splits, int64_t* workspace_bytes) {
+  if (!plan || !splits || !workspace_bytes) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  int s = *splits == 0 ? ccl::recommended_splits(p) : *splits;
+  if (s < 1 || s > ccl::kMaxSplits)
+    return fail(CCL_ERR_INVALID_ARG, "splits must be 0 (choose) or in 1..16");
+  if (ccl_status st = check_split_grid(p, s)) return st;
+  *splits = ccl::effective_splits(p, s);
+  *workspace_bytes = ccl::splitk_workspace_bytes(p, s);
+  return ok();
+}
+
+ccl_status ccl_gemm_splitk(ccl_plan_t plan, float alpha, const void* A_ccl, const void* B_ccl,
+                           float beta, void* C_ccl, int splits, void* workspace,
+                           int64_t workspace_bytes, void* stream) {
+  if (!plan || !A_ccl || !B_ccl || !C_ccl) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  if (splits < 1 || splits > ccl::kMaxSplits)
+    return fail(CCL_ERR_INVALID_ARG, "splits must be in 1..16");
+  if (ccl::effective_splits(p, splits) == 1)
+    return ccl_gemm_scaled(plan, alpha, A_ccl, B_ccl, beta, C_ccl, stream);
+  if (ccl_status st = check_split_grid(p, splits)) return st;
+  if (!workspace) return fail(CCL_ERR_INVALID_ARG, "NULL workspace");
+  if (workspace_bytes < ccl::splitk_workspace_bytes(p, splits))
+    return fail(CCL_ERR_INVALID_ARG, "workspace smaller than ccl_gemm_splitk_workspace reports");
+  if (!aligned16(A_ccl) || !aligned16(B_ccl) || !aligned16(C_ccl) || !aligned16(workspace))
+    return fail(CCL_ERR_MISALIGNED_POINTER, "A, B, C and the workspace must be 16-byte aligned");
+  ccl::OperandAddr a, b, c;
+  ccl_addressing(p, &a, &b, &c);
+  if (!offsets_fit(p, a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
+  if (!addressing_in_bounds(p, a, b, c, p.lay[ccl::OP_A].total_bytes, p.lay[ccl::OP_B].total_bytes,
+                            p.lay[ccl::OP_C].total_bytes))
+    return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the CCL buffers");
+  if (ccl_status s = check_device()) return s;
+  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, alpha, beta, splits,
+                                     static_cast<float*>(workspace), static_cast<hipStream_t>(stream)),
+                    "split-K gemm launch");
 }
 
 ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
@@ -236,7 +286,7 @@ ccl_status ccl_gemm_rowmajor(ccl_plan_t plan, const void* A, const void* B, void
                             p.M * p.N * p.lay[ccl::OP_C].elem_bytes))
     return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the operands");
   if (ccl_status s = check_device()) return s;
-  return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1, 1.f, 0.f,
+  return hip_status(ccl::launch_gemm(p, A, B, C, a, b, c, remap == 1, 1.f, 0.f, 1, nullptr,
                                      static_cast<hipStream_t>(stream)),
                     "gemm launch");
 }

@@ -322,10 +322,50 @@ Traffic remote_bytes(const Plan& p, Placement pl, int flags) {
   return t;
 }
 
-TileMap tile_map(const Plan& p) {
+TileMap tile_map(const Plan& p, int splits) {
   const GemmConfig& g = p.gemm;
+  const int64_t per_xcd = (g.tiles_m * g.tiles_n * splits + g.xcd_per_chiplet - 1) / g.xcd_per_chiplet;
   return TileMap{g.xcd_per_chiplet, p.Gc, (int32_t)g.tiles_m, (int32_t)g.tiles_n,
-                 (int32_t)g.tiles_per_xcd, g.group_m};
+                 (int32_t)per_xcd, g.group_m, splits};
+}
+
+int64_t gemm_ksteps(const Plan& p) {
+  return p.K / (p.ab_type == DT_FP8_E4M3 ? kGemmBK8 : kGemmBK);
+}
+
+int recommended_splits(const Plan& p) {
+  const GemmConfig& g = p.gemm;
+  if (!g.supported) return 1;
+  // Fill the XCD's 32 CUs when its partition has few tiles, keeping at
+  // least 8 K steps per split.
+  const int64_t per_xcd = g.tiles_per_xcd;
+  int s = (int)std::max<int64_t>(1, 32 / std::max<int64_t>(1, per_xcd));
+  s = (int)std::min<int64_t>(s, std::max<int64_t>(1, gemm_ksteps(p) / 8));
+  return std::min(s, kMaxSplits);
+}
+
+int effective_splits(const Plan& p, int splits) {
+  const int64_t ks = gemm_ksteps(p);
+  if (splits <= 1 || ks <= 1) return 1;
+  const int64_t per = (ks + splits - 1) / splits;
+  return (int)((ks + per - 1) / per);
+}
+
+int64_t splitk_workgroups(const Plan& p, int splits) {
+  const GemmConfig& g = p.gemm;
+  const int64_t tiles = g.tiles_m * g.tiles_n * effective_splits(p, splits);
+  return kNumXcd * ((tiles + g.xcd_per_chiplet - 1) / g.xcd_per_chiplet);
+}
+
+int64_t splitk_reduce_workgroups(const Plan& p) {
+  const GemmConfig& g = p.gemm;
+  return g.workgroups * (g.tile_m * g.tile_n / 1024);
+}
+
+int64_t splitk_workspace_bytes(const Plan& p, int splits) {
+  const GemmConfig& g = p.gemm;
+  const int s = effective_splits(p, splits);
+  return s > 1 ? (int64_t)p.G * g.tiles_m * g.tiles_n * s * g.tile_m * g.tile_n * 4 : 0;
 }
 
 void tile_of_wg(const Plan& p, int64_t wg, int* xcd, int64_t* tile_m, int64_t* tile_n) {

@@ -15,6 +15,7 @@ constexpr int kNumXcd = 8;        // MI355X: 8 XCDs, workgroups dispatched round
 constexpr int kMaxChiplets = 64;
 constexpr int kGemmBK = 32;       // K extent of one GEMM main-loop step (bf16)
 constexpr int kGemmBK8 = 64;      // the same for fp8 operands
+constexpr int kMaxSplits = 16;    // split-K ranges per tile
 
 enum Op { OP_A = 0, OP_B = 1, OP_C = 2 };
 // Element types (Fig. 7 sweeps the data type): A and B share one type.
@@ -96,8 +97,25 @@ constexpr int kTrafficCRead = 4;
 // The remote-byte model under one placement.
 Traffic remote_bytes(const Plan& p, Placement pl, int flags);
 
-// Parameters of the workgroup -> tile map of the GEMM launch.
-TileMap tile_map(const Plan& p);
+// Parameters of the workgroup -> tile map of the GEMM launch (splits > 1:
+// the split-K launch).
+TileMap tile_map(const Plan& p, int splits = 1);
+
+// GEMM main-loop steps over K (32 bf16 or 64 fp8 elements each).
+int64_t gemm_ksteps(const Plan& p);
+
+// Split-K: the split count that fills an XCD's CUs for this plan (1 when
+// the partition already has enough tiles); the number of non-empty K ranges
+// when the K steps are cut into ranges of ceil(steps / splits); and the fp32
+// workspace that needs (tiles x ranges x tile elements x 4 bytes, 0 for one
+// range).
+int recommended_splits(const Plan& p);
+int effective_splits(const Plan& p, int splits);
+int64_t splitk_workspace_bytes(const Plan& p, int splits);
+// Workgroups of the split-K GEMM launch and of its reduce launch (one per
+// 256 x float4 chunk of every tile).
+int64_t splitk_workgroups(const Plan& p, int splits);
+int64_t splitk_reduce_workgroups(const Plan& p);
 
 // Workgroup -> (xcd, kernel tile) of the GEMM launch; tile = (-1, -1) if idle.
 void tile_of_wg(const Plan& p, int64_t wg, int* xcd, int64_t* tile_m, int64_t* tile_n);

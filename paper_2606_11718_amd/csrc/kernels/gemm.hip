@@ -52,6 +52,9 @@ struct GemmParams {
   int32_t epi;          // epilogue: 0 acc, 1 alpha*acc, 2 alpha*acc + beta*C (C read)
   int32_t c_f32;        // C elements are fp32 (else bf16)
   float alpha, beta;
+  int32_t ksteps_per_split;  // K steps of one split (= ksteps without split-K)
+  int32_t splits_total; // split-K ranges per tile (reduce kernel)
+  float* ws;            // split-K: fp32 partial tiles (null: write C directly)
 };
 
 // LDS chunk swizzles (16-byte chunk index XOR a function of the row).
@@ -129,12 +132,16 @@ struct FragSet {
   i16x4 b[TN][2];     // two transposed halves (k 0..3 and 4..7) per B fragment
 };
 
-// The output tile (partition pr, pc; tile ti, tj inside it) of this
-// workgroup: the XCD-aware map, or the native grouped raster over the whole
-// tile grid (XCD-oblivious). False when the workgroup has no tile.
-__device__ __forceinline__ bool tile_of_block(const GemmParams& p, int32_t* pr, int32_t* pc,
-                                              int32_t* ti, int32_t* tj) {
-  if (p.remap) return map_tile(p.map, blockIdx.x, pr, pc, ti, tj);
+// The output tile (partition pr, pc; tile ti, tj inside it) and K range
+// (split) of this workgroup: the XCD-aware map, or the native grouped raster
+// over the whole tile grid (XCD-oblivious). False when the workgroup has no
+// tile. The results depend on blockIdx only; the map's integer divisions run
+// on the vector unit, so they are made wave-uniform explicitly: the operand
+// descriptors built from them must live in scalar registers.
+__device__ __forceinline__ bool tile_of_block_raw(const GemmParams& p, int32_t* pr, int32_t* pc,
+                                                  int32_t* ti, int32_t* tj, int32_t* split) {
+  *split = 0;
+  if (p.remap) return map_tile(p.map, blockIdx.x, pr, pc, ti, tj, split);
   const int32_t TMg = p.map.tiles_m * p.grid_r, TNg = p.map.tiles_n * p.map.grid_c;
   const int32_t t = blockIdx.x;
   if (t >= TMg * TNg) return false;
@@ -150,22 +157,92 @@ __device__ __forceinline__ bool tile_of_block(const GemmParams& p, int32_t* pr, 
   return true;
 }
 
-// Epilogue: lane holds C[m][n .. n+3] of each 32x32 MFMA tile (mt, nt) in
-// acc[mt][nt][4q .. 4q+3]; C = alpha * acc (+ beta * C), stored as bf16
-// (nearest even) or fp32.
-template <int BM, int BN, int TM, int TN, int WM, int WN>
-__device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&acc)[TM][TN],
-                                           int32_t pr, int32_t pc, int32_t ti, int32_t tj, int wm,
-                                           int wn, int lane) {
-  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+__device__ __forceinline__ bool tile_of_block(const GemmParams& p, int32_t* pr, int32_t* pc,
+                                              int32_t* ti, int32_t* tj, int32_t* split) {
+  if (!tile_of_block_raw(p, pr, pc, ti, tj, split)) return false;
+  *pr = __builtin_amdgcn_readfirstlane(*pr);
+  *pc = __builtin_amdgcn_readfirstlane(*pc);
+  *ti = __builtin_amdgcn_readfirstlane(*ti);
+  *tj = __builtin_amdgcn_readfirstlane(*tj);
+  *split = __builtin_amdgcn_readfirstlane(*split);
+  return true;
+}
+
+// Position of K step k0 in an operand's K blocks: the block offset and the
+// element offset inside the block (a block holds kslice elements of K).
+// Integer division has no scalar instruction, so the block index is made
+// wave-uniform explicitly: the operand descriptors built from it must live
+// in scalar registers.
+__device__ __forceinline__ void k_start(const OperandAddr& o, int32_t k_elems, int64_t* slice_off,
+                                        int32_t* kl) {
+  const int32_t kc = __builtin_amdgcn_readfirstlane(k_elems / o.kslice);
+  *slice_off = (int64_t)kc * o.slice;
+  *kl = __builtin_amdgcn_readfirstlane(k_elems - kc * o.kslice);
+}
+
+// Index of tile (pr, pc, ti, tj) among all kernel tiles of C.
+__device__ __forceinline__ int64_t tile_id(const GemmParams& p, int32_t pr, int32_t pc, int32_t ti,
+                                           int32_t tj) {
+  return ((int64_t)(pr * p.map.grid_c + pc) * p.map.tiles_m + ti) * p.map.tiles_n + tj;
+}
+
+// Four consecutive C elements at element index idx: alpha * o (+ beta * C),
+// stored as bf16 (nearest even) or fp32.
+__device__ __forceinline__ void store4(const GemmParams& p, int64_t idx, float* o) {
   const int epi = p.epi;
   const float alpha = p.alpha, beta = p.beta;
-  // alpha * acc (+ beta * old) for the four values; old only read when epi == 2.
-  auto scale = [&](float* o, const float* old) {
+  auto scale = [&](const float* old) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       o[j] = epi == 2 ? __builtin_fmaf(alpha, o[j], beta * old[j]) : alpha * o[j];
   };
+  if (p.c_f32) {
+    float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.C) + idx);
+    if (epi != 0) {
+      float old[4] = {0.f, 0.f, 0.f, 0.f};
+      if (epi == 2) {
+        const float4 c = *dst;
+        old[0] = c.x; old[1] = c.y; old[2] = c.z; old[3] = c.w;
+      }
+      scale(old);
+    }
+    *dst = make_float4(o[0], o[1], o[2], o[3]);
+  } else {
+    uint2* dst = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.C) + idx);
+    if (epi != 0) {
+      uint2 c = make_uint2(0u, 0u);
+      if (epi == 2) c = *dst;
+      const float old[4] = {__uint_as_float(c.x << 16), __uint_as_float(c.x & 0xffff0000u),
+                            __uint_as_float(c.y << 16), __uint_as_float(c.y & 0xffff0000u)};
+      scale(old);
+    }
+    uint2 v;
+    v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
+    v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
+    *dst = v;
+  }
+}
+
+// Position of a lane's four accumulators in the split-K partial tile. The
+// partial is stored in fragment order, so that the 64 lanes of a wave write
+// (and the reduce kernel reads) 1 KB contiguous: float4 number
+// (((wave * TM + mt) * TN + nt) * 4 + q) * 64 + lane, wave = wm * (BN / WN) + wn.
+template <int TM, int TN>
+__device__ __forceinline__ int32_t frag_index(int wave, int mt, int nt, int q, int lane) {
+  return (((wave * TM + mt) * TN + nt) * 4 + q) * 64 + lane;
+}
+
+// Epilogue: lane holds C[m][n .. n+3] of each 32x32 MFMA tile (mt, nt) in
+// acc[mt][nt][4q .. 4q+3]. Without split-K: C = alpha * acc (+ beta * C).
+// With split-K: the fp32 partial tile goes to the workspace at tile
+// tile * splits + split, in fragment order, and the reduce kernel writes C.
+template <int BM, int BN, int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&acc)[TM][TN],
+                                           int32_t pr, int32_t pc, int32_t ti, int32_t tj,
+                                           int32_t split, int wm, int wn, int lane) {
+  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  float* part = p.ws ? p.ws + (tile_id(p, pr, pc, ti, tj) * p.map.splits + split) * (BM * BN) : nullptr;
+  const int wave = wm * (BN / WN) + wn;
 #pragma unroll
   for (int mt = 0; mt < TM; ++mt) {
     const int m = wm * WM + mt * 32 + (lane & 31);
@@ -174,38 +251,55 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&a
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int n = wn * WN + nt * 32 + 8 * q + 4 * (lane >> 5);
-        const int64_t idx = c_tile + (int64_t)m * p.c.ld + n;
         float o[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
-        if (p.c_f32) {
-          float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.C) + idx);
-          if (epi != 0) {
-            float old[4] = {0.f, 0.f, 0.f, 0.f};
-            if (epi == 2) {
-              const float4 c = *dst;
-              old[0] = c.x; old[1] = c.y; old[2] = c.z; old[3] = c.w;
-            }
-            scale(o, old);
-          }
-          *dst = make_float4(o[0], o[1], o[2], o[3]);
-        } else {
-          uint2* dst = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.C) + idx);
-          if (epi != 0) {
-            uint2 c = make_uint2(0u, 0u);
-            if (epi == 2) c = *dst;
-            const float old[4] = {__uint_as_float(c.x << 16), __uint_as_float(c.x & 0xffff0000u),
-                                  __uint_as_float(c.y << 16), __uint_as_float(c.y & 0xffff0000u)};
-            scale(o, old);
-          }
-          uint2 v;
-          v.x = bf16_rne(o[0]) | (bf16_rne(o[1]) << 16);
-          v.y = bf16_rne(o[2]) | (bf16_rne(o[3]) << 16);
-          *dst = v;
-        }
+        if (part)
+          reinterpret_cast<float4*>(part)[frag_index<TM, TN>(wave, mt, nt, q, lane)] =
+              make_float4(o[0], o[1], o[2], o[3]);
+        else
+          store4(p, c_tile + (int64_t)m * p.c.ld + n, o);
       }
     }
   }
+}
+
+// Split-K reduction. Each tile is cut into kChunks chunks of 256 float4
+// (fragment order); workgroup w handles chunk (w >> 3) % kChunks of the tile
+// that workgroup ((w >> 3) / kChunks) * 8 + (w & 7) of the unsplit GEMM
+// computes, so it runs on the XCD that wrote the partials. Each thread sums
+// its float4 over the splits in ascending order and writes C through store4.
+template <int BM, int BN, int WGN>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmParams p) {
+  using T = Tile<BM, BN, WGN>;
+  constexpr int kChunks = BM * BN / (4 * 256);
+  const int64_t slot = blockIdx.x >> 3;
+  const int32_t chunk = (int32_t)(slot % kChunks);
+  int32_t pr, pc, ti, tj, split;
+  if (!map_tile(p.map, ((slot / kChunks) << 3) | (blockIdx.x & 7), &pr, &pc, &ti, &tj, &split))
+    return;
+  const int32_t f = chunk * 256 + threadIdx.x;
+  const int lane = f & 63;
+  int r = f >> 6;
+  const int q = r & 3;
+  r >>= 2;
+  const int nt = r % T::TN;
+  r /= T::TN;
+  const int mt = r % T::TM;
+  const int wave = r / T::TM;
+  const int wm = wave / (BN / T::WN), wn = wave % (BN / T::WN);
+  const int m = wm * T::WM + mt * 32 + (lane & 31);
+  const int n = wn * T::WN + nt * 32 + 8 * q + 4 * (lane >> 5);
+  const int32_t S = p.splits_total;
+  const float4* part = reinterpret_cast<const float4*>(p.ws + tile_id(p, pr, pc, ti, tj) * S * (BM * BN)) + f;
+  float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int s = 0; s < S; ++s) {
+    const float4 v = part[(int64_t)s * (BM * BN / 4)];
+    o[0] += v.x; o[1] += v.y; o[2] += v.z; o[3] += v.w;
+  }
+  const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  store4(p, c_tile + (int64_t)m * p.c.ld + n, o);
 }
 
 template <int BM, int BN, int WGN>
@@ -226,8 +320,11 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
   static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
 
-  int32_t pr, pc, ti, tj;
-  if (!tile_of_block(p, &pr, &pc, &ti, &tj)) return;
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  // K range of this workgroup: steps [k0, k0 + ksteps) (all of K without split-K)
+  const int32_t k0 = __builtin_amdgcn_readfirstlane(split * p.ksteps_per_split);
+  const int32_t ksteps = __builtin_amdgcn_readfirstlane(min(p.ksteps, k0 + p.ksteps_per_split) - k0);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -279,8 +376,10 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   // ---- operand corners; K-slice block advances every kslice columns/rows ----
   const uint16_t* a_base = p.A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
   const uint16_t* b_base = p.B + pc * p.b.part + tj * BN;
-  int64_t a_slice_off = 0, b_slice_off = 0;
-  int32_t a_kl = 0, b_kl = 0;
+  int64_t a_slice_off, b_slice_off;
+  int32_t a_kl, b_kl;
+  k_start(p.a, k0 * kBK, &a_slice_off, &a_kl);
+  k_start(p.b, k0 * kBK, &b_slice_off, &b_kl);
 
   // Descriptors of the next K step to be loaded. With live == false they
   // cover zero bytes: every load is out of range, touches no memory and
@@ -394,7 +493,6 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     substep(f1, nullptr, lA, lB, nA, nB, 0, f0);
   };
 
-  const int32_t ksteps = p.ksteps;
   load_stage(smA0, smB0, 0 < ksteps);
   load_stage(smA1, smB1, 1 < ksteps);
   load_stage(smA2, smB2, 2 < ksteps);
@@ -407,7 +505,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     if (s + 3 < ksteps) step(smA3, smB3, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
-  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, wm, wn, lane);
+  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
 }
 
@@ -480,8 +578,11 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
   __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
   static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
 
-  int32_t pr, pc, ti, tj;
-  if (!tile_of_block(p, &pr, &pc, &ti, &tj)) return;
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  // K range of this workgroup: steps [k0, k0 + ksteps) (all of K without split-K)
+  const int32_t k0 = __builtin_amdgcn_readfirstlane(split * p.ksteps_per_split);
+  const int32_t ksteps = __builtin_amdgcn_readfirstlane(min(p.ksteps, k0 + p.ksteps_per_split) - k0);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -534,8 +635,10 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
 
   const char* a_base = A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
   const char* b_base = B + pc * p.b.part + tj * BN;
-  int64_t a_slice_off = 0, b_slice_off = 0;
-  int32_t a_kl = 0, b_kl = 0;
+  int64_t a_slice_off, b_slice_off;
+  int32_t a_kl, b_kl;
+  k_start(p.a, k0 * kBK8, &a_slice_off, &a_kl);
+  k_start(p.b, k0 * kBK8, &b_slice_off, &b_kl);
 
   struct StageSrc {
     i32x4 ra, rb;
@@ -642,7 +745,6 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
   };
 
   Frags f0, f1;
-  const int32_t ksteps = p.ksteps;
   load_stage(smA0, smB0, 0 < ksteps);
   load_stage(smA1, smB1, 1 < ksteps);
   load_stage(smA2, smB2, 2 < ksteps);
@@ -655,7 +757,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
     if (s + 3 < ksteps) step(f1, f0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
-  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, wm, wn, lane);
+  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
 }
 
@@ -679,9 +781,29 @@ __global__ void __launch_bounds__(64) dispatch_probe_kernel(TileMap map, int32_t
 
 }  // namespace
 
+// Second launch of a split-K GEMM: sum the partials of every tile into C.
+static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t stream) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  gp.map = tile_map(p, 1);
+  const dim3 grid((unsigned)splitk_reduce_workgroups(p));
+  const GemmConfig& g = p.gemm;
+#define CCL_REDUCE(BM_, BN_, WGN_) \
+  hipLaunchKernelGGL((splitk_reduce_kernel<BM_, BN_, WGN_>), grid, dim3(256), 0, stream, gp)
+  if (g.tile_m == 256 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 256) CCL_REDUCE(256, 256, 2);
+  else if (g.tile_m == 256 && g.tile_n == 128) CCL_REDUCE(256, 128, 2);
+  else if (g.tile_m == 128 && g.tile_n == 256) CCL_REDUCE(128, 256, 2);
+  else if (g.tile_m == 128 && g.tile_n == 128) CCL_REDUCE(128, 128, 2);
+  else return hipErrorInvalidValue;
+#undef CCL_REDUCE
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
-                       bool remap, float alpha, float beta, hipStream_t stream) {
+                       bool remap, float alpha, float beta, int splits, float* ws,
+                       hipStream_t stream) {
   const GemmConfig& g = p.gemm;
   GemmParams gp;
   gp.A = static_cast<const uint16_t*>(A);
@@ -691,15 +813,20 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   gp.a = a;
   gp.b = b;
   gp.c = c;
-  gp.map = tile_map(p);
+  if (splits < 1 || (splits > 1 && (!remap || !ws))) return hipErrorInvalidValue;
+  splits = effective_splits(p, splits);      // every K range non-empty
+  gp.map = tile_map(p, splits);
   const bool fp8 = p.ab_type == DT_FP8_E4M3;
   gp.ksteps = (int32_t)(p.K / (fp8 ? kBK8 : kBK));
+  gp.ksteps_per_split = (gp.ksteps + splits - 1) / splits;
+  gp.splits_total = splits;
+  gp.ws = splits > 1 ? ws : nullptr;
   gp.remap = remap ? 1 : 0;
   gp.grid_r = p.Gr;
   gp.alpha = alpha;
   gp.beta = beta;
   gp.epi = beta != 0.f ? 2 : (alpha != 1.f ? 1 : 0);
-  const unsigned wgs = remap ? (unsigned)g.workgroups
+  const unsigned wgs = remap ? (unsigned)(8 * (int64_t)gp.map.tiles_per_xcd)
                              : (unsigned)(g.tiles_m * g.tiles_n * p.G);
   dim3 grid(wgs);
   const int waves = g.waves;
@@ -720,7 +847,7 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
     else
       return hipErrorInvalidValue;
 #undef CCL_LAUNCH8
-    return hipGetLastError();
+    return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
   }
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \
@@ -738,7 +865,7 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   else
     return hipErrorInvalidValue;
 #undef CCL_LAUNCH
-  return hipGetLastError();
+  return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
 }
 
 hipError_t launch_dispatch_probe(const Plan& p, int32_t* out, hipStream_t stream) {

@@ -27,10 +27,12 @@ hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, 
 hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld, void* dst,
                              hipStream_t stream);
 // C = alpha A B + beta C with the given operand addressing; remap =
-// XCD-aware tile map. C is read only when beta != 0.
+// XCD-aware tile map. C is read only when beta != 0. splits > 1 (remap
+// only): split-K into the fp32 workspace ws, then a reduce launch.
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
-                       bool remap, float alpha, float beta, hipStream_t stream);
+                       bool remap, float alpha, float beta, int splits, float* ws,
+                       hipStream_t stream);
 // Dispatch probe with the GEMM grid (4 int32 per workgroup).
 hipError_t launch_dispatch_probe(const Plan& p, int32_t* out, hipStream_t stream);
 

@@ -52,6 +52,14 @@ int main(void) {
          (unsigned long long)lt.misses[1], (unsigned long long)lt.remote[0],
          (unsigned long long)lt.remote[1], (unsigned long long)lt.remote[2]);
   /* error paths: nothing is written, a status and a message come back */
+  ccl_plan_t small = NULL;
+  CHECK(ccl_plan(768, 2048, 4096, 8, 1, 4096, &small));
+  int splits = 0;
+  int64_t ws_bytes = -1;
+  CHECK(ccl_gemm_splitk_workspace(small, &splits, &ws_bytes));
+  printf("splitk %d %lld\n", splits, (long long)ws_bytes);
+  CHECK(ccl_plan_destroy(small));
+
   ccl_plan_t bad = NULL;
   ccl_status s = ccl_plan(256, 500, 256, 4, 2, 4096, &bad);
   printf("err_plan %s %d\n", ccl_status_string(s), bad == NULL);

@@ -63,3 +63,8 @@ def test_error_paths(abi_output):
     assert abi_output["err_null"] == ["CCL_ERR_INVALID_ARG"]
     assert abi_output["err_gemm"] == ["CCL_ERR_INVALID_ARG"]
     assert "ok" in abi_output
+
+
+def test_splitk_workspace_query(abi_output):
+    p = ccl.ccl_plan(768, 2048, 4096, 8, 1, 4096)
+    assert list(map(int, abi_output["splitk"])) == list(ccl.ccl_gemm_splitk_workspace(p, 0))
