@@ -17,9 +17,13 @@
 //  * A (K contiguous) fragments: ds_read_b128. B (N contiguous) fragments:
 //    ds_read_b64_tr_b16, which transposes 16-bit data across each group of
 //    16 lanes (lane l, element j <- lane 4j + l/4, element l%4).
-//  * Matrix cores: v_mfma_f32_32x32x16_bf16 with fp32 accumulators; the
-//    product is formed as C^T tiles so that each lane ends up holding four
-//    consecutive columns of C, written as one 8-byte store (bf16, RNE).
+//  * Matrix cores: v_mfma_f32_16x16x32_bf16 with fp32 accumulators (one
+//    instruction covers a whole K step). Measured on MI355X with random
+//    operands, this shape does about 12 % more work per joule than
+//    32x32x16, which is what counts when the GEMM runs at the socket power
+//    limit. The product is formed as C^T tiles so that each lane ends up
+//    holding four consecutive columns of C, written as one 8-byte store
+//    (bf16, RNE).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -33,6 +37,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
@@ -64,9 +69,12 @@ struct GemmParams {
 // SQ_LDS_BANK_CONFLICT: zero conflicts for this form, while e.g. row mod 4
 // or (row / 2) mod 4 give 2- to 4-way conflicts.)
 __device__ __forceinline__ int swz_a(int row) { return (row >> 2) & 3; }
-// B rows are BN*2 bytes: the 4 rows one 16-lane transpose read touches get
-// disjoint 32-byte (and 64-byte) bank windows.
-__device__ __forceinline__ int swz_b(int row) { return ((row & 3) << 1) ^ ((row & 3) << 2); }
+// B rows are BN*2 bytes (16 or 32 chunks). The 32 lanes of a half-wave of
+// one transposed fragment read touch 8 rows (k = 8g + 4r + j for two
+// neighbouring g, j = 0..3) x 2 neighbouring chunks; XOR-ing the chunk with
+// 2 * ((row & 3) | (row & 8) >> 1) sends these 16 (row, chunk) pairs to 16
+// distinct 16-byte bank slots.
+__device__ __forceinline__ int swz_b(int row) { return ((row & 3) << 1) | (((row >> 3) & 1) << 3); }
 
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -108,13 +116,14 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
   return (vm & 15) | (7 << 4) | ((lgkm & 15) << 8) | (((vm >> 4) & 3) << 14);
 }
 
-// Output tile BM x BN computed by a 2 x WGN grid of waves.
+// Output tile BM x BN computed by a 2 x WGN grid of waves, 16 x 16 MFMA
+// tiles.
 template <int BM, int BN, int WGN>
 struct Tile {
   static constexpr int NW = 2 * WGN;                   // waves per workgroup
   static constexpr int THREADS = 64 * NW;
   static constexpr int WM = BM / 2, WN = BN / WGN;     // wave tile
-  static constexpr int TM = WM / 32, TN = WN / 32;     // MFMA tiles per wave
+  static constexpr int TM = WM / 16, TN = WN / 16;     // MFMA tiles per wave
   static constexpr int A_BYTES = BM * kBK * 2;         // one stage
   static constexpr int B_BYTES = kBK * BN * 2;
   static constexpr int NA = BM / (16 * NW);            // A loads per wave per stage (1 KB each)
@@ -123,13 +132,20 @@ struct Tile {
   static constexpr int NB = BN / (16 * NW);            // B loads per wave per stage
   static constexpr int NL = NA + NB;
   static_assert(NA >= 1 && NB >= 1 && TN >= 1, "tile too small for the wave grid");
+  static_assert(TM % 2 == 0, "the step splits the A fragments in two halves");
+  static_assert(TM * TN * 4 <= 128, "accumulators must fit in 128 VGPRs (two waves per SIMD)");
+  static_assert(BN == 128 || BN == 256, "B swizzle is defined for 16- and 32-chunk rows");
 };
 
-// MFMA operand fragments of one 16-wide kk sub-step: A rows and B columns.
-template <int TM, int TN>
-struct FragSet {
+// MFMA operand fragments of one K step: A rows (8 K each per lane) and B
+// columns (two transposed halves, k 0..3 and 4..7 of the lane's 8).
+template <int TM>
+struct AFrags {
   bf16x8 a[TM];
-  i16x4 b[TN][2];     // two transposed halves (k 0..3 and 4..7) per B fragment
+};
+template <int TN>
+struct BFrags {
+  i16x4 b[TN][2];
 };
 
 // The output tile (partition pr, pc; tile ti, tj inside it) and K range
@@ -223,39 +239,56 @@ __device__ __forceinline__ void store4(const GemmParams& p, int64_t idx, float* 
   }
 }
 
-// Position of a lane's four accumulators in the split-K partial tile. The
-// partial is stored in fragment order, so that the 64 lanes of a wave write
-// (and the reduce kernel reads) 1 KB contiguous: float4 number
-// (((wave * TM + mt) * TN + nt) * 4 + q) * 64 + lane, wave = wm * (BN / WN) + wn.
-template <int TM, int TN>
+// Where a lane's accumulators sit in C. The product is formed as C^T
+// tiles, so with MD x MD MFMA tiles (MD = 16 for bf16, 32 for fp8) lane l
+// holds, for each q < Q, C[row][col(q) .. col(q) + 3] of its tile:
+//   MD = 16: Q = 1, row = l % 16, col = 4 (l / 16);
+//   MD = 32: Q = 4, row = l % 32, col = 8 q + 4 (l / 32).
+template <int MD>
+struct AccLayout {
+  static_assert(MD == 16 || MD == 32, "MFMA tiles are 16x16 or 32x32");
+  static constexpr int Q = MD == 16 ? 1 : 4;
+  __device__ static __forceinline__ int row(int lane) { return lane & (MD - 1); }
+  __device__ static __forceinline__ int col(int lane, int q) {
+    return MD == 16 ? 4 * (lane >> 4) : 8 * q + 4 * (lane >> 5);
+  }
+};
+
+// Position of a lane's four accumulators (group q) in the split-K partial
+// tile. The partial is stored in fragment order, so that the 64 lanes of a
+// wave write (and the reduce kernel reads) 1 KB contiguous: float4 number
+// (((wave * TM + mt) * TN + nt) * Q + q) * 64 + lane, wave = wm * (BN / WN) + wn.
+template <int TM, int TN, int Q>
 __device__ __forceinline__ int32_t frag_index(int wave, int mt, int nt, int q, int lane) {
-  return (((wave * TM + mt) * TN + nt) * 4 + q) * 64 + lane;
+  return (((wave * TM + mt) * TN + nt) * Q + q) * 64 + lane;
 }
 
-// Epilogue: lane holds C[m][n .. n+3] of each 32x32 MFMA tile (mt, nt) in
-// acc[mt][nt][4q .. 4q+3]. Without split-K: C = alpha * acc (+ beta * C).
-// With split-K: the fp32 partial tile goes to the workspace at tile
-// tile * splits + split, in fragment order, and the reduce kernel writes C.
-template <int BM, int BN, int TM, int TN, int WM, int WN>
-__device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&acc)[TM][TN],
+// Epilogue: lane holds C[m][n .. n+3] of each MD x MD MFMA tile (mt, nt) in
+// acc[mt][nt][4q .. 4q+3] (AccLayout). Without split-K: C = alpha * acc
+// (+ beta * C). With split-K: the fp32 partial tile goes to the workspace at
+// tile tile * splits + split, in fragment order, and the reduce kernel
+// writes C.
+template <int BM, int BN, int MD, int TM, int TN, int WM, int WN, typename Acc>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc (&acc)[TM][TN],
                                            int32_t pr, int32_t pc, int32_t ti, int32_t tj,
                                            int32_t split, int wm, int wn, int lane) {
+  using L = AccLayout<MD>;
   const int64_t c_tile = pr * p.c.part + pc * p.c.slice + (int64_t)(ti * BM) * p.c.ld + tj * BN;
   float* part = p.ws ? p.ws + (tile_id(p, pr, pc, ti, tj) * p.map.splits + split) * (BM * BN) : nullptr;
   const int wave = wm * (BN / WN) + wn;
 #pragma unroll
   for (int mt = 0; mt < TM; ++mt) {
-    const int m = wm * WM + mt * 32 + (lane & 31);
+    const int m = wm * WM + mt * MD + L::row(lane);
 #pragma unroll
     for (int nt = 0; nt < TN; ++nt) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = wn * WN + nt * 32 + 8 * q + 4 * (lane >> 5);
+      for (int q = 0; q < L::Q; ++q) {
+        const int n = wn * WN + nt * MD + L::col(lane, q);
         float o[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[j] = acc[mt][nt][4 * q + j];
         if (part)
-          reinterpret_cast<float4*>(part)[frag_index<TM, TN>(wave, mt, nt, q, lane)] =
+          reinterpret_cast<float4*>(part)[frag_index<TM, TN, L::Q>(wave, mt, nt, q, lane)] =
               make_float4(o[0], o[1], o[2], o[3]);
         else
           store4(p, c_tile + (int64_t)m * p.c.ld + n, o);
@@ -269,9 +302,12 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&a
 // that workgroup ((w >> 3) / kChunks) * 8 + (w & 7) of the unsplit GEMM
 // computes, so it runs on the XCD that wrote the partials. Each thread sums
 // its float4 over the splits in ascending order and writes C through store4.
-template <int BM, int BN, int WGN>
+// MD is the MFMA tile of the GEMM kernel that wrote the partials.
+template <int BM, int BN, int WGN, int MD>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmParams p) {
-  using T = Tile<BM, BN, WGN>;
+  using L = AccLayout<MD>;
+  constexpr int WM = BM / 2, WN = BN / WGN;
+  constexpr int TM = WM / MD, TN = WN / MD;
   constexpr int kChunks = BM * BN / (4 * 256);
   const int64_t slot = blockIdx.x >> 3;
   const int32_t chunk = (int32_t)(slot % kChunks);
@@ -281,15 +317,15 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmParams p) {
   const int32_t f = chunk * 256 + threadIdx.x;
   const int lane = f & 63;
   int r = f >> 6;
-  const int q = r & 3;
-  r >>= 2;
-  const int nt = r % T::TN;
-  r /= T::TN;
-  const int mt = r % T::TM;
-  const int wave = r / T::TM;
-  const int wm = wave / (BN / T::WN), wn = wave % (BN / T::WN);
-  const int m = wm * T::WM + mt * 32 + (lane & 31);
-  const int n = wn * T::WN + nt * 32 + 8 * q + 4 * (lane >> 5);
+  const int q = r % L::Q;
+  r /= L::Q;
+  const int nt = r % TN;
+  r /= TN;
+  const int mt = r % TM;
+  const int wave = r / TM;
+  const int wm = wave / (BN / WN), wn = wave % (BN / WN);
+  const int m = wm * WM + mt * MD + L::row(lane);
+  const int n = wn * WN + nt * MD + L::col(lane, q);
   const int32_t S = p.splits_total;
   const float4* part = reinterpret_cast<const float4*>(p.ws + tile_id(p, pr, pc, ti, tj) * S * (BM * BN)) + f;
   float o[4] = {0.f, 0.f, 0.f, 0.f};
@@ -352,12 +388,13 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   const int32_t b_extent = (kBK - 1) * p.b.ld * 2 + BN * 2;
 
   // ---- LDS fragment read offsets (bytes) ----
-  int32_t a_rd[2];
+  // A fragment of MFMA tile mt: lane l reads row wm*WM + 16 mt + l % 16,
+  // K chunk l / 16 (8 bf16). B fragment of tile nt, half r: lane l = 16 g + s
+  // reads 4 columns of row 8 g + 4 r + s / 4 for the transposed read.
+  int32_t a_rd;
   {
-    const int row = wm * T::WM + (lane & 31);
-    const int h = lane >> 5;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) a_rd[kk] = row * 64 + (((2 * kk + h) ^ swz_a(row)) * 16);
+    const int row = wm * T::WM + (lane & 15);
+    a_rd = row * 64 + (((lane >> 4) ^ swz_a(row)) * 16);
   }
   int32_t b_rd[T::TN][2];
   {
@@ -366,8 +403,8 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     for (int nt = 0; nt < T::TN; ++nt) {
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
-        const int krow = 8 * (g >> 1) + 4 * r + (s >> 2);
-        const int col = wn * T::WN + nt * 32 + 16 * (g & 1) + 4 * (s & 3);
+        const int krow = 8 * g + 4 * r + (s >> 2);
+        const int col = wn * T::WN + nt * 16 + 4 * (s & 3);
         b_rd[nt][r] = krow * (BN * 2) + (((col >> 3) ^ swz_b(krow)) * 16) + ((col >> 2) & 1) * 8;
       }
     }
@@ -416,64 +453,37 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     for (int i = 0; i < T::NL; ++i) load_one(d, smA, smB, i);
   };
 
-  using Frags = FragSet<T::TM, T::TN>;
-  constexpr int kReadsPerKK = T::TM + 2 * T::TN;
-  // LDS read i (0 .. kReadsPerKK-1) of the kk sub-step's fragments.
-  auto read_one = [&](const char* smA, const char* smB, int kk, Frags& f, int i) {
-    if (i < T::TM) {
-      f.a[i] = *(const lds_bf16x8*)(smA + a_rd[kk] + i * 32 * 64);
-    } else {
-      const int nt = (i - T::TM) >> 1, r = (i - T::TM) & 1;
-      f.b[nt][r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(smB + b_rd[nt][r] + kk * 16 * BN * 2));
-    }
+  constexpr int kHalfM = T::TM / 2;               // A fragments per half step
+  AFrags<T::TM> fa;
+  BFrags<T::TN> fb0, fb1;
+  auto read_a = [&](const char* smA, int mt) {
+    fa.a[mt] = *(const lds_bf16x8*)(smA + a_rd + mt * 16 * 64);
   };
-  auto read_frags = [&](const char* smA, const char* smB, int kk, Frags& f) {
-#pragma unroll
-    for (int i = 0; i < kReadsPerKK; ++i) read_one(smA, smB, kk, f, i);
+  // B read i (0 .. 2 TN - 1): tile i / 2, half i % 2.
+  auto read_b = [&](const char* smB, BFrags<T::TN>& fb, int i) {
+    const int nt = i >> 1, r = i & 1;
+    fb.b[nt][r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(smB + b_rd[nt][r]));
   };
 
-  f32x16 acc[T::TM][T::TN];
+  f32x4 acc[T::TM][T::TN];
 #pragma unroll
   for (int i = 0; i < T::TM; ++i)
 #pragma unroll
     for (int j = 0; j < T::TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
 
-  constexpr int kMfmaPerKK = T::TM * T::TN;
-  auto mfma_one = [&](const Frags& f, int i) {
-    const int mt = i / T::TN, nt = i % T::TN;
-    const bf16x8 b = __builtin_bit_cast(
-        bf16x8, __builtin_shufflevector(f.b[nt][0], f.b[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
-    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, f.a[mt], acc[mt][nt], 0, 0, 0);
-  };
-  // One kk sub-step: MFMAs on f, each followed by at most one direct-to-LDS
-  // load of a later stage (when d is given) and one LDS read of the next
-  // fragments into g. The order is pinned so the matrix pipe always has
-  // the next MFMA ready while the memory instructions drain behind it.
-  auto substep = [&](const Frags& f, const StageSrc* d, char* lA, char* lB, const char* rA,
-                     const char* rB, int rkk, Frags& g) {
-#pragma unroll
-    for (int i = 0; i < kMfmaPerKK; ++i) {
-      mfma_one(f, i);
-      if (d && i < T::NL) load_one(*d, lA, lB, i);
-      if (i < kReadsPerKK) read_one(rA, rB, rkk, g, i);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int i = kMfmaPerKK; i < kReadsPerKK; ++i) read_one(rA, rB, rkk, g, i);
-#pragma unroll
-    for (int i = kMfmaPerKK; i < T::NL; ++i)
-      if (d) load_one(*d, lA, lB, i);
-    __builtin_amdgcn_sched_barrier(0);
+  auto mfma_one = [&](const BFrags<T::TN>& fb, int mt, int nt) {
+    const bf16x8 bv = __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(fb.b[nt][0], fb.b[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
+    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv, fa.a[mt], acc[mt][nt], 0, 0, 0);
   };
 
   // Wait for the own loads of the next stage (the later stages' loads stay
-  // in flight), then for every wave: after this barrier the next stage is
-  // complete in LDS, and nobody reads the stage that the next load reuses.
-  // An LDS-only wait: a full fence would also wait for the in-flight
-  // direct-to-LDS loads of the later stages.
+  // in flight) and for this wave's LDS reads, then for every wave: after
+  // this barrier the next stage is complete in LDS, and nobody reads the
+  // stage that the next load reuses. An LDS-only wait: a full fence would
+  // also wait for the in-flight direct-to-LDS loads of the later stages.
   auto stage_barrier = [&]() {
     __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * T::NL, 0));
     asm volatile("" ::: "memory");
@@ -481,31 +491,67 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     asm volatile("" ::: "memory");
   };
 
-  Frags f0, f1;
-  // One K step on stage (smA, smB), whose kk = 0 fragments are in f0. The
-  // step kStages-1 ahead is loaded into (lA, lB); the next stage (nA, nB)
-  // is waited for, and its kk = 0 fragments are read into f0.
-  auto step = [&](const char* smA, const char* smB, char* lA, char* lB, const char* nA,
-                  const char* nB, bool live) {
+  // One K step on stage (smA, smB). On entry A fragments 0 .. kHalfM-1 and
+  // the B fragments fb hold this stage's data. First half: the MFMAs of A
+  // fragments 0 .. kHalfM-1, each followed by at most one memory
+  // instruction: the reads of A fragments kHalfM .. TM-1 of this stage, then
+  // the direct-to-LDS loads of the step kStages-1 ahead into (lA, lB). After
+  // the stage barrier, the second half runs the MFMAs of A fragments
+  // kHalfM .. TM-1 and reads the next stage (nA, nB): A fragments
+  // 0 .. kHalfM-1 (no longer needed) and all B fragments into fbn. The order
+  // is pinned so the matrix pipe always has the next MFMA ready while the
+  // memory instructions drain behind it.
+  auto step = [&](const char* smA, const char* smB, const BFrags<T::TN>& fb, BFrags<T::TN>& fbn,
+                  char* lA, char* lB, const char* nA, const char* nB, bool live) {
     const StageSrc d = next_src(live);
-    substep(f0, &d, lA, lB, smA, smB, 1, f1);
+    constexpr int kMfmaHalf = kHalfM * T::TN;
+    constexpr int kOps1 = kHalfM + T::NL;
+#pragma unroll
+    for (int i = 0; i < kMfmaHalf; ++i) {
+      mfma_one(fb, i / T::TN, i % T::TN);
+      if (i < kHalfM) read_a(smA, kHalfM + i);
+      else if (i < kOps1) load_one(d, lA, lB, i - kHalfM);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfmaHalf; i < kOps1; ++i) {
+      if (i < kHalfM) read_a(smA, kHalfM + i);
+      else load_one(d, lA, lB, i - kHalfM);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     stage_barrier();
-    substep(f1, nullptr, lA, lB, nA, nB, 0, f0);
+    constexpr int kOps2 = kHalfM + 2 * T::TN;
+#pragma unroll
+    for (int i = 0; i < kMfmaHalf; ++i) {
+      mfma_one(fb, kHalfM + i / T::TN, i % T::TN);
+      if (i < kHalfM) read_a(nA, i);
+      else if (i < kOps2) read_b(nB, fbn, i - kHalfM);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfmaHalf; i < kOps2; ++i) {
+      if (i < kHalfM) read_a(nA, i);
+      else read_b(nB, fbn, i - kHalfM);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   load_stage(smA0, smB0, 0 < ksteps);
   load_stage(smA1, smB1, 1 < ksteps);
   load_stage(smA2, smB2, 2 < ksteps);
   stage_barrier();
-  read_frags(smA0, smB0, 0, f0);
+#pragma unroll
+  for (int mt = 0; mt < kHalfM; ++mt) read_a(smA0, mt);
+#pragma unroll
+  for (int i = 0; i < 2 * T::TN; ++i) read_b(smB0, fb0, i);
   for (int32_t s = 0; s < ksteps; s += kStages) {
-    step(smA0, smB0, smA3, smB3, smA1, smB1, s + 3 < ksteps);
-    if (s + 1 < ksteps) step(smA1, smB1, smA0, smB0, smA2, smB2, s + 4 < ksteps);
-    if (s + 2 < ksteps) step(smA2, smB2, smA1, smB1, smA3, smB3, s + 5 < ksteps);
-    if (s + 3 < ksteps) step(smA3, smB3, smA2, smB2, smA0, smB0, s + 6 < ksteps);
+    step(smA0, smB0, fb0, fb1, smA3, smB3, smA1, smB1, s + 3 < ksteps);
+    if (s + 1 < ksteps) step(smA1, smB1, fb1, fb0, smA0, smB0, smA2, smB2, s + 4 < ksteps);
+    if (s + 2 < ksteps) step(smA2, smB2, fb0, fb1, smA1, smB1, smA3, smB3, s + 5 < ksteps);
+    if (s + 3 < ksteps) step(smA3, smB3, fb1, fb0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
-  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
 }
 
@@ -757,7 +803,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
     if (s + 3 < ksteps) step(f1, f0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
   }
 
-  store_tile<BM, BN, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  store_tile<BM, BN, 32, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
 }
 
@@ -788,14 +834,20 @@ static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t
   gp.map = tile_map(p, 1);
   const dim3 grid((unsigned)splitk_reduce_workgroups(p));
   const GemmConfig& g = p.gemm;
-#define CCL_REDUCE(BM_, BN_, WGN_) \
-  hipLaunchKernelGGL((splitk_reduce_kernel<BM_, BN_, WGN_>), grid, dim3(256), 0, stream, gp)
-  if (g.tile_m == 256 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE(256, 256, 4);
-  else if (g.tile_m == 256 && g.tile_n == 256) CCL_REDUCE(256, 256, 2);
-  else if (g.tile_m == 256 && g.tile_n == 128) CCL_REDUCE(256, 128, 2);
-  else if (g.tile_m == 128 && g.tile_n == 256) CCL_REDUCE(128, 256, 2);
-  else if (g.tile_m == 128 && g.tile_n == 128) CCL_REDUCE(128, 128, 2);
+  // The partials are in the fragment order of the kernel that wrote them:
+  // 16x16 MFMA tiles for bf16, 32x32 for fp8.
+  const int md = p.ab_type == DT_FP8_E4M3 ? 32 : 16;
+#define CCL_REDUCE(BM_, BN_, WGN_, MD_) \
+  hipLaunchKernelGGL((splitk_reduce_kernel<BM_, BN_, WGN_, MD_>), grid, dim3(256), 0, stream, gp)
+#define CCL_REDUCE_MD(BM_, BN_, WGN_) \
+  do { if (md == 16) CCL_REDUCE(BM_, BN_, WGN_, 16); else CCL_REDUCE(BM_, BN_, WGN_, 32); } while (0)
+  if (g.tile_m == 256 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE_MD(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 256 && md == 32) CCL_REDUCE(256, 256, 2, 32);
+  else if (g.tile_m == 256 && g.tile_n == 128) CCL_REDUCE_MD(256, 128, 2);
+  else if (g.tile_m == 128 && g.tile_n == 256) CCL_REDUCE_MD(128, 256, 2);
+  else if (g.tile_m == 128 && g.tile_n == 128) CCL_REDUCE_MD(128, 128, 2);
   else return hipErrorInvalidValue;
+#undef CCL_REDUCE_MD
 #undef CCL_REDUCE
   return hipGetLastError();
 }
@@ -852,10 +904,10 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \
                      stream, gp)
+  // bf16 256x256 tiles always run 8 waves (the 4-wave form would need 256
+  // accumulator registers per lane).
   if (g.tile_m == 256 && g.tile_n == 256 && waves == 8)
     CCL_LAUNCH(256, 256, 4);
-  else if (g.tile_m == 256 && g.tile_n == 256)
-    CCL_LAUNCH(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128)
     CCL_LAUNCH(256, 128, 2);
   else if (g.tile_m == 128 && g.tile_n == 256)
