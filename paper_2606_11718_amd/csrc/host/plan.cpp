@@ -99,13 +99,11 @@ void choose_gemm_config(Plan* p) {
   int gm = 4;
   if (const char* e = std::getenv("CCL_GEMM_GROUP_M")) gm = std::max(1, std::atoi(e));
   g.group_m = (int)std::min<int64_t>(gm, g.tiles_m);
-  // 256x256 tiles run with 8 waves (two per SIMD). For fp8 operands
-  // CCL_GEMM_WAVES=4 selects the 4-wave form of the same kernel; the bf16
-  // kernel has no 4-wave 256x256 form (its 16x16 MFMA tiles would need 256
-  // accumulator registers per lane).
+  // 256x256 tiles run with 8 waves (two per SIMD) by default; CCL_GEMM_WAVES=4
+  // selects the 4-wave form of the same kernel.
   g.waves = (btm == 256 && btn == 256) ? 8 : 4;
   if (const char* e = std::getenv("CCL_GEMM_WAVES"))
-    if (p->ab_type == DT_FP8_E4M3 && btm == 256 && btn == 256) g.waves = std::atoi(e) == 4 ? 4 : 8;
+    g.waves = (std::atoi(e) == 8 && btm == 256 && btn == 256) ? 8 : 4;
   if (g.workgroups > 0x7fffffff) {
     g.why_unsupported = "launch too large";
     return;

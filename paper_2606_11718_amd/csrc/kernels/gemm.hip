@@ -43,7 +43,13 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
 constexpr int kBK = 32;          // K extent of one main-loop step
-constexpr int kStages = 4;       // LDS stages; loads run kStages-1 steps ahead
+constexpr int kStages = 4;       // fp8 LDS stages; loads run kStages-1 steps ahead
+// bf16 LDS stages (32 KiB each for a 256x256 tile); loads run kStagesBf16-1
+// steps ahead.
+#ifndef CCL_BF16_STAGES
+#define CCL_BF16_STAGES 4
+#endif
+constexpr int kStagesBf16 = CCL_BF16_STAGES;
 
 struct GemmParams {
   const uint16_t* A;
@@ -63,14 +69,21 @@ struct GemmParams {
 };
 
 // LDS chunk swizzles (16-byte chunk index XOR a function of the row).
-// A rows are 64 B (4 chunks): chunk slot = logical chunk XOR (row / 4) mod 4,
-// so the 16 rows a quarter-wave reads at one logical chunk fill all 16
-// 16-byte columns of a 256-byte bank row. (Measured on gfx950 with
-// SQ_LDS_BANK_CONFLICT: zero conflicts for this form, while e.g. row mod 4
-// or (row / 2) mod 4 give 2- to 4-way conflicts.)
+// Bank model of gfx950, measured with SQ_LDS_BANK_CONFLICT on single-lane
+// pairs: 64 banks of 4 bytes; an 8-byte read (ds_read_b64, also the
+// transposing form) serves each half-wave in one cycle; ds_read_b128 serves
+// a half-wave in two cycles, split by the parity of lane bits 2..4 (lanes
+// 0-3, 12-15, 20-23, 24-27 together). A read is conflict-free when the
+// lanes of each such group touch distinct banks.
+//
+// A rows are 64 B (4 chunks). swz_a serves the fp8 kernel's A reads (32
+// rows x 2 chunks per half-wave): chunk XOR (row / 4) mod 4. swz_a16 serves
+// the bf16 kernel's 16x16 A reads (16 rows x 4 chunks per wave): chunk XOR
+// 2 * (bit 2 of row). Both measure zero conflicts.
 __device__ __forceinline__ int swz_a(int row) { return (row >> 2) & 3; }
+__device__ __forceinline__ int swz_a16(int row) { return ((row >> 2) & 1) << 1; }
 // B rows are BN*2 bytes (16 or 32 chunks). The 32 lanes of a half-wave of
-// one transposed fragment read touch 8 rows (k = 8g + 4r + j for two
+// one bf16 transposed fragment read touch 8 rows (k = 8g + 4r + j for two
 // neighbouring g, j = 0..3) x 2 neighbouring chunks; XOR-ing the chunk with
 // 2 * ((row & 3) | (row & 8) >> 1) sends these 16 (row, chunk) pairs to 16
 // distinct 16-byte bank slots.
@@ -133,7 +146,7 @@ struct Tile {
   static constexpr int NL = NA + NB;
   static_assert(NA >= 1 && NB >= 1 && TN >= 1, "tile too small for the wave grid");
   static_assert(TM % 2 == 0, "the step splits the A fragments in two halves");
-  static_assert(TM * TN * 4 <= 128, "accumulators must fit in 128 VGPRs (two waves per SIMD)");
+  static_assert(TM * TN * 4 <= 256, "accumulators must fit in 256 registers per lane");
   static_assert(BN == 128 || BN == 256, "B swizzle is defined for 16- and 32-chunk rows");
 };
 
@@ -344,17 +357,9 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   // buffer-resource builtins.
 #if defined(__HIP_DEVICE_COMPILE__)
   using T = Tile<BM, BN, WGN>;
-  // One array per stage, so that the compiler tracks the direct-to-LDS
-  // writes of each stage separately.
-  __shared__ __attribute__((aligned(1024))) char smA0[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA1[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA2[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA3[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB0[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB1[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB2[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
-  static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
+  constexpr int NS = kStagesBf16;
+  __shared__ __attribute__((aligned(1024))) char smA[NS][T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[NS][T::B_BYTES];
 
   int32_t pr, pc, ti, tj, split;
   if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
@@ -373,7 +378,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 #pragma unroll
   for (int i = 0; i < T::NA; ++i) {
     const int row = 16 * (wave * T::NA + i) + (lane >> 2);
-    const int chunk = (lane & 3) ^ swz_a(row);
+    const int chunk = (lane & 3) ^ swz_a16(row);
     a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
   }
   uint32_t b_voff[T::NB];
@@ -394,7 +399,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   int32_t a_rd;
   {
     const int row = wm * T::WM + (lane & 15);
-    a_rd = row * 64 + (((lane >> 4) ^ swz_a(row)) * 16);
+    a_rd = row * 64 + (((lane >> 4) ^ swz_a16(row)) * 16);
   }
   int32_t b_rd[T::TN][2];
   {
@@ -485,7 +490,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   // stage that the next load reuses. An LDS-only wait: a full fence would
   // also wait for the in-flight direct-to-LDS loads of the later stages.
   auto stage_barrier = [&]() {
-    __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * T::NL, 0));
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((NS - 2) * T::NL, 0));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -495,7 +500,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   // the B fragments fb hold this stage's data. First half: the MFMAs of A
   // fragments 0 .. kHalfM-1, each followed by at most one memory
   // instruction: the reads of A fragments kHalfM .. TM-1 of this stage, then
-  // the direct-to-LDS loads of the step kStages-1 ahead into (lA, lB). After
+  // the direct-to-LDS loads of the step NS-1 ahead into (lA, lB). After
   // the stage barrier, the second half runs the MFMAs of A fragments
   // kHalfM .. TM-1 and reads the next stage (nA, nB): A fragments
   // 0 .. kHalfM-1 (no longer needed) and all B fragments into fbn. The order
@@ -536,20 +541,35 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  load_stage(smA0, smB0, 0 < ksteps);
-  load_stage(smA1, smB1, 1 < ksteps);
-  load_stage(smA2, smB2, 2 < ksteps);
+  // Prologue: the first NS-1 stages in flight, then stage 0's first fragments.
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) load_stage(smA[j], smB[j], j < ksteps);
   stage_barrier();
 #pragma unroll
-  for (int mt = 0; mt < kHalfM; ++mt) read_a(smA0, mt);
+  for (int mt = 0; mt < kHalfM; ++mt) read_a(smA[0], mt);
 #pragma unroll
-  for (int i = 0; i < 2 * T::TN; ++i) read_b(smB0, fb0, i);
-  for (int32_t s = 0; s < ksteps; s += kStages) {
-    step(smA0, smB0, fb0, fb1, smA3, smB3, smA1, smB1, s + 3 < ksteps);
-    if (s + 1 < ksteps) step(smA1, smB1, fb1, fb0, smA0, smB0, smA2, smB2, s + 4 < ksteps);
-    if (s + 2 < ksteps) step(smA2, smB2, fb0, fb1, smA1, smB1, smA3, smB3, s + 5 < ksteps);
-    if (s + 3 < ksteps) step(smA3, smB3, fb1, fb0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
+  for (int i = 0; i < 2 * T::TN; ++i) read_b(smB[0], fb0, i);
+  // Steps run in rounds of kRound (a multiple of NS and of the two B
+  // fragment sets): step j of a round works on stage j % NS, loads stage
+  // (j + NS - 1) % NS and reads stage (j + 1) % NS. Whole rounds run in a
+  // branch-free loop (the compiler then tracks the outstanding LDS reads
+  // exactly and waits only for the fragments each MFMA needs); the last,
+  // partial round runs its steps under conditions.
+  constexpr int kRound = NS % 2 ? 2 * NS : NS;
+  auto round_step = [&](int j, int32_t s) {
+    step(smA[j % NS], smB[j % NS], j % 2 ? fb1 : fb0, j % 2 ? fb0 : fb1,
+         smA[(j + NS - 1) % NS], smB[(j + NS - 1) % NS], smA[(j + 1) % NS],
+         smB[(j + 1) % NS], s + j + NS - 1 < ksteps);
+  };
+  const int32_t full = ksteps - ksteps % kRound;
+  int32_t s = 0;
+  for (; s < full; s += kRound) {
+#pragma unroll
+    for (int j = 0; j < kRound; ++j) round_step(j, s);
   }
+#pragma unroll
+  for (int j = 0; j < kRound - 1; ++j)
+    if (s + j < ksteps) round_step(j, s);
 
   store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
@@ -842,7 +862,7 @@ static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t
 #define CCL_REDUCE_MD(BM_, BN_, WGN_) \
   do { if (md == 16) CCL_REDUCE(BM_, BN_, WGN_, 16); else CCL_REDUCE(BM_, BN_, WGN_, 32); } while (0)
   if (g.tile_m == 256 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE_MD(256, 256, 4);
-  else if (g.tile_m == 256 && g.tile_n == 256 && md == 32) CCL_REDUCE(256, 256, 2, 32);
+  else if (g.tile_m == 256 && g.tile_n == 256) CCL_REDUCE_MD(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128) CCL_REDUCE_MD(256, 128, 2);
   else if (g.tile_m == 128 && g.tile_n == 256) CCL_REDUCE_MD(128, 256, 2);
   else if (g.tile_m == 128 && g.tile_n == 128) CCL_REDUCE_MD(128, 128, 2);
@@ -904,10 +924,10 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \
                      stream, gp)
-  // bf16 256x256 tiles always run 8 waves (the 4-wave form would need 256
-  // accumulator registers per lane).
   if (g.tile_m == 256 && g.tile_n == 256 && waves == 8)
     CCL_LAUNCH(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 256)
+    CCL_LAUNCH(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128)
     CCL_LAUNCH(256, 128, 2);
   else if (g.tile_m == 128 && g.tile_n == 256)
