@@ -64,6 +64,7 @@ struct GemmParams {
   int32_t c_f32;        // C elements are fp32 (else bf16)
   float alpha, beta;
   int32_t ksteps_per_split;  // K steps of one split (= ksteps without split-K)
+  int32_t round_fast;   // bf16: K blocks and split starts are 4-step aligned (rounds path)
   int32_t splits_total; // split-K ranges per tile (reduce kernel)
   float* ws;            // split-K: fp32 partial tiles (null: write C directly)
 };
@@ -121,6 +122,13 @@ __device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t voff, const char*
   const uint32_t m0v = (uint32_t)(uintptr_t)(const lds_char*)lds;
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :: "s"(m0v), "v"(voff), "s"(rsrc) : "m0");
+}
+// The same with a scalar byte offset added to the memory address (the LDS
+// destination is unchanged).
+__device__ __forceinline__ void lds_dma16_so(i32x4 rsrc, uint32_t voff, uint32_t soff, const char* lds) {
+  const uint32_t m0v = (uint32_t)(uintptr_t)(const lds_char*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "m0");
 }
 #pragma clang diagnostic pop
 
@@ -422,6 +430,16 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   int32_t a_kl, b_kl;
   k_start(p.a, k0 * kBK, &a_slice_off, &a_kl);
   k_start(p.b, k0 * kBK, &b_slice_off, &b_kl);
+  // Byte address of the next K step's A and B corners. It advances by one
+  // step at a time; after the last step of a CCL K block it jumps to the
+  // start of the next block.
+  const char* a_next = reinterpret_cast<const char*>(a_base + a_slice_off + a_kl);
+  const char* b_next = reinterpret_cast<const char*>(b_base + b_slice_off + (int64_t)b_kl * p.b.ld);
+  const int32_t a_steps = p.a.kslice / kBK, b_steps = p.b.kslice / kBK;   // steps per block
+  int32_t a_left = a_steps - a_kl / kBK, b_left = b_steps - b_kl / kBK;   // left in this block
+  const int64_t a_adv = kBK * 2, b_adv = (int64_t)kBK * p.b.ld * 2;
+  const int64_t a_jump = (p.a.slice - p.a.kslice) * 2;
+  const int64_t b_jump = (p.b.slice - (int64_t)p.b.kslice * p.b.ld) * 2;
 
   // Descriptors of the next K step to be loaded. With live == false they
   // cover zero bytes: every load is out of range, touches no memory and
@@ -431,31 +449,56 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   };
   auto next_src = [&](bool live) {
     StageSrc d;
-    d.ra = buffer_rsrc(a_base + a_slice_off + a_kl, live ? a_extent : 0);
-    d.rb = buffer_rsrc(b_base + b_slice_off + (int64_t)b_kl * p.b.ld, live ? b_extent : 0);
+    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
     // advance to the next K step (branch-free; past the last step the
     // corners are only used with empty descriptors)
-    a_kl += kBK;
-    const bool a_wrap = a_kl == p.a.kslice;
-    a_kl = a_wrap ? 0 : a_kl;
-    a_slice_off += a_wrap ? p.a.slice : 0;
-    b_kl += kBK;
-    const bool b_wrap = b_kl == p.b.kslice;
-    b_kl = b_wrap ? 0 : b_kl;
-    b_slice_off += b_wrap ? p.b.slice : 0;
+    const bool a_wrap = --a_left == 0;
+    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left;
+    const bool b_wrap = --b_left == 0;
+    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left;
     return d;
   };
-  // Load i (0 .. NL-1) of this wave for one stage.
-  auto load_one = [&](const StageSrc& d, char* smA, char* smB, int i) {
-    if (i < T::NA)
-      lds_dma16(d.ra, a_voff[i], smA + (wave * T::NA + i) * 1024);
-    else
-      lds_dma16(d.rb, b_voff[i - T::NA], smB + (wave * T::NB + (i - T::NA)) * 1024);
+  // Descriptors of four consecutive K steps at once (the rounds path): the
+  // steps of a round address their K slice through the loads' scalar
+  // offsets (so_a[j], so_b[j]); the corners advance by four steps. Only
+  // used where no round straddles a CCL K block (a_left is then a multiple
+  // of 4 here, or the operand has a single block).
+  const int32_t a_extent4 = (BM - 1) * p.a.ld * 2 + 4 * kBK * 2;
+  const int32_t b_extent4 = (4 * kBK - 1) * p.b.ld * 2 + BN * 2;
+  const uint32_t so_a[4] = {0u, (uint32_t)a_adv, (uint32_t)(2 * a_adv), (uint32_t)(3 * a_adv)};
+  const uint32_t so_b[4] = {0u, (uint32_t)b_adv, (uint32_t)(2 * b_adv), (uint32_t)(3 * b_adv)};
+  auto round_src = [&]() {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_next, a_extent4);
+    d.rb = buffer_rsrc(b_next, b_extent4);
+    const bool a_wrap = a_left == 4;
+    a_next += 4 * a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left - 4;
+    const bool b_wrap = b_left == 4;
+    b_next += 4 * b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left - 4;
+    return d;
+  };
+  // Load i (0 .. NL-1) of this wave for one stage; j >= 0 selects the
+  // scalar offsets of step j of a round.
+  auto load_one = [&](const StageSrc& d, int j, char* smA, char* smB, int i) {
+    if (i < T::NA) {
+      char* dst = smA + (wave * T::NA + i) * 1024;
+      if (j < 0) lds_dma16(d.ra, a_voff[i], dst);
+      else lds_dma16_so(d.ra, a_voff[i], so_a[j], dst);
+    } else {
+      char* dst = smB + (wave * T::NB + (i - T::NA)) * 1024;
+      if (j < 0) lds_dma16(d.rb, b_voff[i - T::NA], dst);
+      else lds_dma16_so(d.rb, b_voff[i - T::NA], so_b[j], dst);
+    }
   };
   auto load_stage = [&](char* smA, char* smB, bool live) {
     const StageSrc d = next_src(live);
 #pragma unroll
-    for (int i = 0; i < T::NL; ++i) load_one(d, smA, smB, i);
+    for (int i = 0; i < T::NL; ++i) load_one(d, -1, smA, smB, i);
   };
 
   constexpr int kHalfM = T::TM / 2;               // A fragments per half step
@@ -507,21 +550,20 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   // is pinned so the matrix pipe always has the next MFMA ready while the
   // memory instructions drain behind it.
   auto step = [&](const char* smA, const char* smB, const BFrags<T::TN>& fb, BFrags<T::TN>& fbn,
-                  char* lA, char* lB, const char* nA, const char* nB, bool live) {
-    const StageSrc d = next_src(live);
+                  char* lA, char* lB, const char* nA, const char* nB, const StageSrc& d, int j) {
     constexpr int kMfmaHalf = kHalfM * T::TN;
     constexpr int kOps1 = kHalfM + T::NL;
 #pragma unroll
     for (int i = 0; i < kMfmaHalf; ++i) {
       mfma_one(fb, i / T::TN, i % T::TN);
       if (i < kHalfM) read_a(smA, kHalfM + i);
-      else if (i < kOps1) load_one(d, lA, lB, i - kHalfM);
+      else if (i < kOps1) load_one(d, j, lA, lB, i - kHalfM);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int i = kMfmaHalf; i < kOps1; ++i) {
       if (i < kHalfM) read_a(smA, kHalfM + i);
-      else load_one(d, lA, lB, i - kHalfM);
+      else load_one(d, j, lA, lB, i - kHalfM);
     }
     __builtin_amdgcn_sched_barrier(0);
     stage_barrier();
@@ -549,27 +591,48 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   for (int mt = 0; mt < kHalfM; ++mt) read_a(smA[0], mt);
 #pragma unroll
   for (int i = 0; i < 2 * T::TN; ++i) read_b(smB[0], fb0, i);
-  // Steps run in rounds of kRound (a multiple of NS and of the two B
-  // fragment sets): step j of a round works on stage j % NS, loads stage
-  // (j + NS - 1) % NS and reads stage (j + 1) % NS. Whole rounds run in a
-  // branch-free loop (the compiler then tracks the outstanding LDS reads
-  // exactly and waits only for the fragments each MFMA needs); the last,
-  // partial round runs its steps under conditions.
-  constexpr int kRound = NS % 2 ? 2 * NS : NS;
-  auto round_step = [&](int j, int32_t s) {
-    step(smA[j % NS], smB[j % NS], j % 2 ? fb1 : fb0, j % 2 ? fb0 : fb1,
-         smA[(j + NS - 1) % NS], smB[(j + NS - 1) % NS], smA[(j + 1) % NS],
-         smB[(j + 1) % NS], s + j + NS - 1 < ksteps);
+  // Step s works on stage s % NS, loads stage (s + NS - 1) % NS (the step
+  // NS-1 ahead) and reads stage (s + 1) % NS; the B fragment sets alternate.
+  // ph is s modulo a multiple of NS and of 2, known at compile time.
+  auto phase_step = [&](int ph, const StageSrc& d, int j) {
+    step(smA[ph % NS], smB[ph % NS], ph % 2 ? fb1 : fb0, ph % 2 ? fb0 : fb1,
+         smA[(ph + NS - 1) % NS], smB[(ph + NS - 1) % NS], smA[(ph + 1) % NS],
+         smB[(ph + 1) % NS], d, j);
   };
-  const int32_t full = ksteps - ksteps % kRound;
+  // One step with its own descriptors (live: the step it loads exists).
+  auto single_step = [&](int ph, int32_t s) {
+    const StageSrc d = next_src(s + NS - 1 < ksteps);
+    phase_step(ph, d, -1);
+  };
+  constexpr int kRound = NS % 2 ? 2 * NS : NS;
   int32_t s = 0;
-  for (; s < full; s += kRound) {
+  if (NS == 4 && p.round_fast) {
+    // Rounds path. Step 0 alone; then rounds of 4 steps (s = 1 mod 4) whose
+    // loads (steps s+3 .. s+6, a 4-aligned group) are all live and share
+    // one pair of descriptors; the remaining steps (at most 6) alone. Whole
+    // rounds run branch-free, so the compiler tracks the outstanding LDS
+    // reads exactly and waits only for the fragments each MFMA needs.
+    single_step(0, 0);
+    for (s = 1; s + 7 <= ksteps; s += 4) {
+      const StageSrc d = round_src();
 #pragma unroll
-    for (int j = 0; j < kRound; ++j) round_step(j, s);
+      for (int j = 0; j < 4; ++j) phase_step(1 + j, d, j);
+    }
+#pragma unroll
+    for (int t = 0; t < 6; ++t)
+      if (s + t < ksteps) single_step(1 + t, s + t);
+  } else {
+    // Per-step path: whole rounds of kRound steps branch-free, then the
+    // last, partial round under conditions.
+    const int32_t full = ksteps - ksteps % kRound;
+    for (; s < full; s += kRound) {
+#pragma unroll
+      for (int j = 0; j < kRound; ++j) single_step(j, s + j);
+    }
+#pragma unroll
+    for (int j = 0; j < kRound - 1; ++j)
+      if (s + j < ksteps) single_step(j, s + j);
   }
-#pragma unroll
-  for (int j = 0; j < kRound - 1; ++j)
-    if (s + j < ksteps) round_step(j, s);
 
   store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
@@ -891,6 +954,15 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   const bool fp8 = p.ab_type == DT_FP8_E4M3;
   gp.ksteps = (int32_t)(p.K / (fp8 ? kBK8 : kBK));
   gp.ksteps_per_split = (gp.ksteps + splits - 1) / splits;
+  // Rounds path of the bf16 kernel: each operand's K blocks are a multiple
+  // of 4 steps (or it has one block), and every split starts 4-aligned.
+  {
+    const auto aligned = [&](const OperandAddr& o) {
+      return (int64_t)o.kslice == p.K || (o.kslice / kBK) % 4 == 0;
+    };
+    gp.round_fast = (!fp8 && kStagesBf16 == 4 && aligned(a) && aligned(b) &&
+                     (splits == 1 || gp.ksteps_per_split % 4 == 0)) ? 1 : 0;
+  }
   gp.splits_total = splits;
   gp.ws = splits > 1 ? ws : nullptr;
   gp.remap = remap ? 1 : 0;
