@@ -697,15 +697,9 @@ template <int BM, int BN, int WGN>
 __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)
   using T = Tile8<BM, BN, WGN>;
-  __shared__ __attribute__((aligned(1024))) char smA0[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA1[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA2[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smA3[T::A_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB0[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB1[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB2[T::B_BYTES];
-  __shared__ __attribute__((aligned(1024))) char smB3[T::B_BYTES];
-  static_assert(kStages == 4, "stage arrays are spelled out for 4 stages");
+  constexpr int NS = kStages;
+  __shared__ __attribute__((aligned(1024))) char smA[NS][T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[NS][T::B_BYTES];
 
   int32_t pr, pc, ti, tj, split;
   if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
@@ -769,33 +763,44 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
   k_start(p.a, k0 * kBK8, &a_slice_off, &a_kl);
   k_start(p.b, k0 * kBK8, &b_slice_off, &b_kl);
 
+  // Byte address of the next K step's A and B corners; one step at a time,
+  // with a jump to the next CCL K block after a block's last step.
+  const char* a_next = a_base + a_slice_off + a_kl;
+  const char* b_next = b_base + b_slice_off + (int64_t)b_kl * p.b.ld;
+  const int32_t a_steps = p.a.kslice / kBK8, b_steps = p.b.kslice / kBK8;   // steps per block
+  int32_t a_left = a_steps - a_kl / kBK8, b_left = b_steps - b_kl / kBK8;   // left in this block
+  const int64_t a_adv = kBK8, b_adv = (int64_t)kBK8 * p.b.ld;
+  const int64_t a_jump = p.a.slice - p.a.kslice;
+  const int64_t b_jump = p.b.slice - (int64_t)p.b.kslice * p.b.ld;
+
+  // Descriptors of the next K step to be loaded. With live == false they
+  // cover zero bytes: every load is out of range, touches no memory and
+  // writes zeros to the (unused) stage.
   struct StageSrc {
     i32x4 ra, rb;
   };
   auto next_src = [&](bool live) {
     StageSrc d;
-    d.ra = buffer_rsrc(a_base + a_slice_off + a_kl, live ? a_extent : 0);
-    d.rb = buffer_rsrc(b_base + b_slice_off + (int64_t)b_kl * p.b.ld, live ? b_extent : 0);
-    a_kl += kBK8;
-    const bool a_wrap = a_kl == p.a.kslice;
-    a_kl = a_wrap ? 0 : a_kl;
-    a_slice_off += a_wrap ? p.a.slice : 0;
-    b_kl += kBK8;
-    const bool b_wrap = b_kl == p.b.kslice;
-    b_kl = b_wrap ? 0 : b_kl;
-    b_slice_off += b_wrap ? p.b.slice : 0;
+    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
+    const bool a_wrap = --a_left == 0;
+    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left;
+    const bool b_wrap = --b_left == 0;
+    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left;
     return d;
   };
-  auto load_one = [&](const StageSrc& d, char* smA, char* smB, int i) {
+  auto load_one = [&](const StageSrc& d, char* sA, char* sB, int i) {
     if (i < T::NA)
-      lds_dma16(d.ra, a_voff[i], smA + (wave * T::NA + i) * 1024);
+      lds_dma16(d.ra, a_voff[i], sA + (wave * T::NA + i) * 1024);
     else
-      lds_dma16(d.rb, b_voff[i - T::NA], smB + (wave * T::NB + (i - T::NA)) * 1024);
+      lds_dma16(d.rb, b_voff[i - T::NA], sB + (wave * T::NB + (i - T::NA)) * 1024);
   };
-  auto load_stage = [&](char* smA, char* smB, bool live) {
+  auto load_stage = [&](char* sA, char* sB, bool live) {
     const StageSrc d = next_src(live);
 #pragma unroll
-    for (int i = 0; i < T::NL; ++i) load_one(d, smA, smB, i);
+    for (int i = 0; i < T::NL; ++i) load_one(d, sA, sB, i);
   };
 
   using Frags = FragSet8<T::TM, T::TN>;
@@ -843,19 +848,19 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
   };
 
   // One K step on the stage whose fragments are in f: the first half of the
-  // MFMAs issues the loads of the step kStages-1 ahead into (lA, lB); after
-  // the barrier the second half reads the next stage's (nA, nB) fragments
-  // into g. The fragment sets alternate between steps.
+  // MFMAs issues the loads of the step NS-1 ahead into (lA, lB) with the
+  // descriptors d; after the barrier the second half
+  // reads the next stage's (nA, nB) fragments into g. The fragment sets
+  // alternate between steps.
   auto step = [&](const Frags& f, Frags& g, char* lA, char* lB, const char* nA, const char* nB,
-                  bool live) {
-    const StageSrc d = next_src(live);
+                  const StageSrc& d) {
 #pragma unroll
     for (int i = 0; i < kHalf; ++i) {
       mfma_one(f, i);
       const int per = (T::NL + kHalf - 1) / kHalf;
 #pragma unroll
-      for (int j = 0; j < per; ++j)
-        if (i * per + j < T::NL) load_one(d, lA, lB, i * per + j);
+      for (int q = 0; q < per; ++q)
+        if (i * per + q < T::NL) load_one(d, lA, lB, i * per + q);
       __builtin_amdgcn_sched_barrier(0);
     }
     stage_barrier();
@@ -865,8 +870,8 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
     for (int i = 0; i < rest; ++i) {
       mfma_one(f, kHalf + i);
 #pragma unroll
-      for (int j = 0; j < per; ++j)
-        if (i * per + j < kReads) read_one(nA, nB, g, i * per + j);
+      for (int q = 0; q < per; ++q)
+        if (i * per + q < kReads) read_one(nA, nB, g, i * per + q);
       __builtin_amdgcn_sched_barrier(0);
     }
     if constexpr (rest == 0) read_frags(nA, nB, g);
@@ -874,17 +879,31 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
   };
 
   Frags f0, f1;
-  load_stage(smA0, smB0, 0 < ksteps);
-  load_stage(smA1, smB1, 1 < ksteps);
-  load_stage(smA2, smB2, 2 < ksteps);
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) load_stage(smA[j], smB[j], j < ksteps);
   stage_barrier();
-  read_frags(smA0, smB0, f0);
-  for (int32_t s = 0; s < ksteps; s += kStages) {
-    step(f0, f1, smA3, smB3, smA1, smB1, s + 3 < ksteps);
-    if (s + 1 < ksteps) step(f1, f0, smA0, smB0, smA2, smB2, s + 4 < ksteps);
-    if (s + 2 < ksteps) step(f0, f1, smA1, smB1, smA3, smB3, s + 5 < ksteps);
-    if (s + 3 < ksteps) step(f1, f0, smA2, smB2, smA0, smB0, s + 6 < ksteps);
+  read_frags(smA[0], smB[0], f0);
+  // Step s works on stage s % NS, loads stage (s + NS - 1) % NS and reads
+  // stage (s + 1) % NS; ph is s modulo NS (a multiple of 2). Whole rounds of
+  // NS steps run branch-free (so the compiler tracks the outstanding LDS
+  // reads exactly); the last, partial round runs its steps under conditions.
+  // (The bf16 kernel's rounds path, one descriptor per four steps, needs
+  // more scalar registers than this kernel has left.)
+  static_assert(NS % 2 == 0, "fragment sets alternate by step parity");
+  auto single_step = [&](int ph, int32_t s) {
+    const StageSrc d = next_src(s + NS - 1 < ksteps);
+    step(ph % 2 ? f1 : f0, ph % 2 ? f0 : f1, smA[(ph + NS - 1) % NS], smB[(ph + NS - 1) % NS],
+         smA[(ph + 1) % NS], smB[(ph + 1) % NS], d);
+  };
+  int32_t s = 0;
+  const int32_t full = ksteps - ksteps % NS;
+  for (; s < full; s += NS) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) single_step(j, s + j);
   }
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j)
+    if (s + j < ksteps) single_step(j, s + j);
 
   store_tile<BM, BN, 32, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
