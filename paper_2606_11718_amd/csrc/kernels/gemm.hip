@@ -909,6 +909,228 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8_kernel(GemmParams
 #endif
 }
 
+// ---------------------------------------------------------------------------
+// fp8 (E4M3) operands on v_mfma_f32_16x16x128_f8f6f4 (unscaled). One
+// instruction covers a whole 128-wide K step, so a stage holds 128 K: A rows
+// of 128 bytes and B rows of BN bytes x 128 rows, 64 KiB for a 256x256 tile.
+// Two stages: the loads of step t+1 are issued at the start of step t,
+// right after the barrier that frees their stage.
+//
+// K order inside an instruction: lane l (16-lane group g = l / 16) holds 32
+// bytes; byte p < 16 is K = 16 g + p and byte p >= 16 is K = 64 + 16 g +
+// (p - 16). A and B use the same order, so every product pairs equal K.
+// A fragment: 16-byte chunks g and 4 + g of a 128-byte row (two
+// ds_read_b128). B fragment: four ds_read_b64_tr_b8, rows 16 g + 8 r and
+// 64 + 16 g + 8 r, each giving 8 consecutive K of the lane's column.
+// ---------------------------------------------------------------------------
+
+constexpr int kBK8x = 128;       // K extent of one step of gemm_fp8x_kernel
+
+template <int BM, int BN, int WGN>
+struct Tile8x {
+  static constexpr int NW = 2 * WGN;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int A_BYTES = BM * kBK8x;           // one stage
+  static constexpr int B_BYTES = kBK8x * BN;
+  static constexpr int NA = A_BYTES / (1024 * NW);     // 8 A rows of 128 B per load
+  static constexpr int CPR_B = BN / 16;                // 16-byte chunks per B row
+  static constexpr int RPI_B = 64 / CPR_B;             // B rows per load instruction
+  static constexpr int NB = B_BYTES / (1024 * NW);
+  static constexpr int NL = NA + NB;
+  static_assert(NA >= 1 && NB >= 1 && TN >= 2 && TM >= 2, "tile too small for the wave grid");
+  static_assert(BN == 128 || BN == 256, "B swizzle is defined for 128- and 256-byte rows");
+  static_assert(TM * TN * 4 <= 128, "accumulators must fit in 128 VGPRs (two waves per SIMD)");
+};
+
+// Swizzles, conflict-free under the measured bank model: A (128-byte rows,
+// 16 rows x 2 chunks per ds_read_b128 half-wave pair): chunk XOR (row & 6).
+// B (BN-byte rows; a half-wave of one transposed read touches 16 rows x one
+// 16-byte chunk): 256-byte rows XOR (row & 7) | 8 bit4(row); 128-byte rows
+// XOR (row >> 1 & 3) | 4 bit4(row).
+__device__ __forceinline__ int swz_a8x(int row) { return row & 6; }
+template <int BN>
+__device__ __forceinline__ int swz_b8x(int row) {
+  return BN == 256 ? ((row & 7) | (((row >> 4) & 1) << 3)) : (((row >> 1) & 3) | (((row >> 4) & 1) << 2));
+}
+
+template <int BM, int BN, int WGN>
+__global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8x_kernel(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using T = Tile8x<BM, BN, WGN>;
+  __shared__ __attribute__((aligned(1024))) char smA[2][T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[2][T::B_BYTES];
+
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  const int32_t k0 = __builtin_amdgcn_readfirstlane(split * p.ksteps_per_split);
+  const int32_t ksteps = __builtin_amdgcn_readfirstlane(min(p.ksteps, k0 + p.ksteps_per_split) - k0);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  // ---- global -> LDS (byte offsets from the K step's tile corner) ----
+  uint32_t a_voff[T::NA];
+#pragma unroll
+  for (int i = 0; i < T::NA; ++i) {
+    const int row = 8 * (wave * T::NA + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz_a8x(row);
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 16);
+  }
+  uint32_t b_voff[T::NB];
+#pragma unroll
+  for (int i = 0; i < T::NB; ++i) {
+    const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
+    const int chunk = (lane % T::CPR_B) ^ swz_b8x<BN>(row);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 16);
+  }
+  const int32_t a_extent = (BM - 1) * p.a.ld + kBK8x;
+  const int32_t b_extent = (kBK8x - 1) * p.b.ld + BN;
+
+  // ---- LDS fragment read offsets (bytes); A tile mt adds mt * 16 rows ----
+  int32_t a_rd[2];
+  {
+    const int row = wm * T::WM + (lane & 15);
+    const int g = lane >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) a_rd[h] = row * kBK8x + (((4 * h + g) ^ swz_a8x(row)) * 16);
+  }
+  int32_t b_rd[T::TN][4];
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int nt = 0; nt < T::TN; ++nt) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int krow = 64 * (r >> 1) + 16 * g + 8 * (r & 1) + (s >> 1);
+        const int col = wn * T::WN + nt * 16 + 8 * (s & 1);
+        b_rd[nt][r] = krow * BN + (((col >> 4) ^ swz_b8x<BN>(krow)) * 16) + (col & 15);
+      }
+    }
+  }
+
+  // ---- operand corners (see the bf16 kernel) ----
+  const char* A = reinterpret_cast<const char*>(p.A);
+  const char* B = reinterpret_cast<const char*>(p.B);
+  const char* a_base = A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
+  const char* b_base = B + pc * p.b.part + tj * BN;
+  int64_t a_slice_off, b_slice_off;
+  int32_t a_kl, b_kl;
+  k_start(p.a, k0 * kBK8x, &a_slice_off, &a_kl);
+  k_start(p.b, k0 * kBK8x, &b_slice_off, &b_kl);
+  const char* a_next = a_base + a_slice_off + a_kl;
+  const char* b_next = b_base + b_slice_off + (int64_t)b_kl * p.b.ld;
+  const int32_t a_steps = p.a.kslice / kBK8x, b_steps = p.b.kslice / kBK8x;
+  int32_t a_left = a_steps - a_kl / kBK8x, b_left = b_steps - b_kl / kBK8x;
+  const int64_t a_adv = kBK8x, b_adv = (int64_t)kBK8x * p.b.ld;
+  const int64_t a_jump = p.a.slice - p.a.kslice;
+  const int64_t b_jump = p.b.slice - (int64_t)p.b.kslice * p.b.ld;
+  struct StageSrc {
+    i32x4 ra, rb;
+  };
+  auto next_src = [&](bool live) {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
+    const bool a_wrap = --a_left == 0;
+    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left;
+    const bool b_wrap = --b_left == 0;
+    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left;
+    return d;
+  };
+  auto load_one = [&](const StageSrc& d, char* sA, char* sB, int i) {
+    if (i < T::NA)
+      lds_dma16(d.ra, a_voff[i], sA + (wave * T::NA + i) * 1024);
+    else
+      lds_dma16(d.rb, b_voff[i - T::NA], sB + (wave * T::NB + (i - T::NA)) * 1024);
+  };
+
+  i32x8 fa[2];             // A fragments of tiles mt (fa[mt % 2]) and mt + 1
+  i32x8 fb[T::TN];
+  auto read_a_half = [&](const char* sA, int mt, int h, i32x8& f) {
+    const i32x4v v = *(const lds_i32x4*)(sA + a_rd[h] + mt * 16 * kBK8x);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) f[4 * h + q] = v[q];
+  };
+  auto read_b = [&](const char* sB, int i) {     // i = 4 nt + r
+    const int nt = i >> 2, r = i & 3;
+    const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(sB + b_rd[nt][r]));
+    fb[nt][2 * r] = v[0];
+    fb[nt][2 * r + 1] = v[1];
+  };
+
+  f32x4 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+
+  // Wait for the own loads of this step's stage, then for every wave: the
+  // stage is complete in LDS and nobody still reads the other stage.
+  auto step_barrier = [&]() {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // One K step on stage st: first the loads of step t+1 into stage st ^ 1
+  // (a whole step before they are needed), interleaved with the reads of
+  // A tile 0 and all B fragments; then the MFMAs tile row by tile row, with
+  // the reads of the next A tile (into the other A buffer) behind them.
+  auto step = [&](int st, bool live_next) {
+    const StageSrc d = next_src(live_next);
+    const char* sA = smA[st];
+    const char* sB = smB[st];
+    constexpr int kFirst = 2 + 4 * T::TN;          // reads before the first MFMA
+#pragma unroll
+    for (int i = 0; i < (kFirst > T::NL ? kFirst : T::NL); ++i) {
+      if (i < T::NL) load_one(d, smA[st ^ 1], smB[st ^ 1], i);
+      if (i < 2) read_a_half(sA, 0, i, fa[0]);
+      else if (i < kFirst) read_b(sB, i - 2);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int mt = 0; mt < T::TM; ++mt) {
+#pragma unroll
+      for (int nt = 0; nt < T::TN; ++nt) {
+        acc[mt][nt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fb[nt], fa[mt & 1], acc[mt][nt],
+                                                                       0, 0, 0, 0, 0, 0);
+        if (nt < 2 && mt + 1 < T::TM) read_a_half(sA, mt + 1, nt, fa[(mt + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  {
+    const StageSrc d = next_src(0 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d, smA[0], smB[0], i);
+  }
+  // Steps in pairs (stages 0, 1) branch-free, then a last odd step.
+  int32_t t = 0;
+  for (; t + 2 <= ksteps; t += 2) {
+    step_barrier();
+    step(0, t + 1 < ksteps);
+    step_barrier();
+    step(1, t + 2 < ksteps);
+  }
+  if (t < ksteps) {
+    step_barrier();
+    step(0, false);
+  }
+
+  store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+#endif
+}
+
 // Records, per workgroup of the GEMM grid, the XCD it ran on and its tile.
 __global__ void __launch_bounds__(64) dispatch_probe_kernel(TileMap map, int32_t tiles_m,
                                                             int32_t tiles_n, int32_t* out) {
@@ -993,6 +1215,17 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                              : (unsigned)(g.tiles_m * g.tiles_n * p.G);
   dim3 grid(wgs);
   const int waves = g.waves;
+  // fp8 on 256x256 tiles with 8 waves: the 16x16x128 kernel, where every
+  // K block is a multiple of its 128-wide step (no split-K). Other fp8
+  // plans run the 32x32x64 kernel.
+  if (fp8 && splits == 1 && waves == 8 && g.tile_m == 256 && g.tile_n == 256 &&
+      a.kslice % kBK8x == 0 && b.kslice % kBK8x == 0) {
+    gp.ksteps = (int32_t)(p.K / kBK8x);
+    gp.ksteps_per_split = gp.ksteps;
+    hipLaunchKernelGGL((gemm_fp8x_kernel<256, 256, 4>), grid, dim3(Tile8x<256, 256, 4>::THREADS), 0,
+                       stream, gp);
+    return hipGetLastError();
+  }
   if (fp8) {
 #define CCL_LAUNCH8(BM_, BN_, WGN_)                                                    \
   hipLaunchKernelGGL((gemm_fp8_kernel<BM_, BN_, WGN_>), grid, dim3(Tile8<BM_, BN_, WGN_>::THREADS), \

@@ -83,6 +83,9 @@ def _logical(stored, trans):
     (4096, 768, 2048, 8, 8, 0, 1),               # Qwen3 dH shape (B stored transposed)
     (1024, 1024, 576, 1, 1, 0, 0),               # 9 K steps: ragged against the 4-stage loop
     (128, 128, 64, 1, 1, 0, 0),                  # one tile, one K step
+    (1024, 1024, 640, 1, 1, 0, 0),               # 16x16x128 kernel: 5 steps of 128 (odd)
+    (2048, 2048, 1024, 8, 2, 1, 1),              # 16x16x128 kernel: both stored transposed,
+                                                 # K blocks of 2 (A) and 4 (B) steps
 ])
 @pytest.mark.parametrize("c_type", [ccl.CCL_DT_BF16, ccl.CCL_DT_FP32])
 def test_fp8_gemm_matches_oracle(M, N, K, G, Gr, ta, tb, c_type):
