@@ -35,8 +35,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama_fwd_traffic.json")
 GEMM_SRC = os.path.join(ROOT, "paper_2606_11718_amd", "csrc", "kernels", "gemm.hip")
 
 
-def kernel_hash() -> str:
-    return hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()[:16]
+def kernel_hash(src: str = GEMM_SRC) -> str:
+    """Hash of the GEMM source with comments and whitespace removed, so that
+    only a change to the code itself retires the committed counters."""
+    import re
+    text = open(src, encoding="utf-8").read()
+    text = re.sub(r"//[^\n]*", "", text)
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = "".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
 def measured_traffic(launch_flops_unused=None):

@@ -2,7 +2,14 @@
 // III-C: the arithmetic is the plain tiled GEMM; only the operand address
 // map is CCL's).
 //
-// Workgroup = 2 x WGN waves, output tile BM x BN, K step 32 (kBK).
+// Three kernels share the tile map, the operand descriptors, the
+// direct-to-LDS loads and the epilogue:
+//  * gemm_kernel: bf16 operands (described below);
+//  * gemm_fp8x_kernel: fp8 operands on 256x256 tiles with 8 waves and K
+//    blocks that are multiples of 128 (v_mfma_f32_16x16x128_f8f6f4);
+//  * gemm_fp8_kernel: the other fp8 plans (v_mfma_f32_32x32x64_f8f6f4).
+//
+// bf16: workgroup = 2 x WGN waves, output tile BM x BN, K step 32 (kBK).
 //  * Workgroup -> tile: tile_map.hpp. Dispatch is round-robin over the 8
 //    XCDs, so the map sends every tile to an XCD of the chiplet that owns
 //    it (Sec. III-A).
@@ -57,7 +64,7 @@ struct GemmParams {
   void* C;                // bf16, or fp32 when c_f32
   OperandAddr a, b, c;
   TileMap map;
-  int32_t ksteps;       // K / 32
+  int32_t ksteps;       // K / (the kernel's K step)
   int32_t remap;        // 1: XCD-aware map; 0: native raster over the whole C
   int32_t grid_r;       // Gr (native raster)
   int32_t epi;          // epilogue: 0 acc, 1 alpha*acc, 2 alpha*acc + beta*C (C read)
