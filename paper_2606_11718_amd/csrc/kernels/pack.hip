@@ -72,10 +72,13 @@ __device__ __forceinline__ void st(T* p, T v) {
 
 // U = unit moved per access: one 16-byte vector, or one element (1, 2 or 4
 // bytes) when rows are not 16-byte multiples. UNPACK = false: row-major ->
-// CCL; true: CCL -> row-major. NT: streaming accesses, used for tensors
-// larger than the 256 MiB Infinity Cache (measured: +10 % on a 470 MB copy,
-// -15 % on a 134 MB one).
-template <typename U, bool UNPACK, bool NT>
+// CCL; true: CCL -> row-major. NTL / NTS: streaming (non-temporal) loads /
+// stores, used for tensors larger than the 256 MiB Infinity Cache
+// (measured: +10 % on a 470 MB copy, -15 % on a 134 MB one that the cache
+// holds). Below that size, plain stores let the packed operand land in the
+// Infinity Cache: streaming stores made the 134 MB activation pack 12 %
+// slower between the FFN GEMMs.
+template <typename U, bool UNPACK, bool NTL, bool NTS>
 __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
   const int32_t b = blockIdx.y;                      // strip / chiplet
   const int64_t pr = b / a.grid_c, pc = b % a.grid_c;
@@ -99,9 +102,9 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       rm_off[u] = (int64_t)row * a.ld_bytes + (int64_t)col * US;
       if (ok[u]) {
         if (UNPACK)
-          v[u] = ld<NT>(reinterpret_cast<const U*>(a.ccl + strip_base + (int64_t)q * US));
+          v[u] = ld<NTL>(reinterpret_cast<const U*>(a.ccl + strip_base + (int64_t)q * US));
         else
-          v[u] = ld<NT>(reinterpret_cast<const U*>(src_rm + rm_off[u]));
+          v[u] = ld<NTL>(reinterpret_cast<const U*>(src_rm + rm_off[u]));
       }
     }
 #pragma unroll
@@ -109,15 +112,17 @@ __global__ void __launch_bounds__(256) copy_kernel(PackArgs a) {
       const uint32_t q = base + threadIdx.x + u * 256u;
       if (ok[u]) {
         if (UNPACK)
-          st<NT>(reinterpret_cast<U*>(dst_rm + rm_off[u]), v[u]);
+          st<NTS>(reinterpret_cast<U*>(dst_rm + rm_off[u]), v[u]);
         else
-          st<NT>(reinterpret_cast<U*>(a.ccl_out + strip_base + (int64_t)q * US), v[u]);
+          st<NTS>(reinterpret_cast<U*>(a.ccl_out + strip_base + (int64_t)q * US), v[u]);
       }
     }
   }
 }
 
-// Stored-transpose pack: src holds X^T (cols x rows, leading dimension ld
+// Stored-transpose pack through LDS, for blocks whose sides are multiples of
+// 64 but not of the register kernel's block edge below (fp8 blocks with a
+// side of 64 mod 128): src holds X^T (cols x rows, leading dimension ld
 // elements), X is rows x cols of element type E. A 64 x 64 tile is read
 // along X's rows (contiguous in src) in 16-byte chunks, transposed through
 // LDS and written in 16-byte chunks along X's columns (contiguous in the
@@ -167,6 +172,46 @@ __global__ void __launch_bounds__(256) pack_trans_kernel(TransArgs a) {
   }
 }
 
+// Stored-transpose pack without LDS. With EPC elements per 16-byte chunk,
+// each thread moves an EPC x EPC block: it reads EPC chunks, one from each
+// of EPC consecutive rows of the stored transpose, transposes the block in
+// registers (byte permutes) and writes EPC chunks along consecutive rows of
+// the CCL strip. Lane (a, b) = (lane % 8, lane / 8) covers X rows
+// R0 + EPC a .. + EPC - 1 and X columns C0 + EPC b .. + EPC - 1, so a wave
+// covers a WB x WB block (WB = 8 EPC) and each of its loads and stores
+// touches 8 rows x 128 contiguous bytes. The 4 waves of a workgroup take 4
+// consecutive blocks along X's columns. Blocks never straddle CCL blocks
+// (hr and wc are multiples of WB). NTL: streaming loads (sources beyond the
+// Infinity Cache). The stores always stream: on a 134 MB transpose that
+// measured +12 % from HBM and no loss with the source cache-resident.
+template <typename E, bool NTL>
+__global__ void __launch_bounds__(256) pack_trans_reg_kernel(TransArgs a, int32_t wb_cols) {
+  constexpr int EPC = 16 / (int)sizeof(E);
+  constexpr int WB = 8 * EPC;
+  typedef E ev __attribute__((ext_vector_type(EPC)));
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int32_t wcb = blockIdx.x * 4 + wave;
+  if (wcb >= wb_cols) return;
+  const int la = lane & 7, lb = lane >> 3;
+  const int64_t R0 = (int64_t)blockIdx.y * WB, C0 = (int64_t)wcb * WB;
+  const E* src = reinterpret_cast<const E*>(a.src) + (C0 + EPC * lb) * a.ld + R0 + EPC * la;
+  ev in[EPC];
+#pragma unroll
+  for (int j = 0; j < EPC; ++j)
+    in[j] = __builtin_bit_cast(ev, ld<NTL>(reinterpret_cast<const u32x4*>(src + j * a.ld)));
+  const int32_t pr = (int32_t)(R0 / a.hr), pc = (int32_t)(C0 / a.wc);
+  E* strip = reinterpret_cast<E*>(a.dst + ((int64_t)pr * a.grid_c + pc) * a.strip);
+  E* dst = strip + (R0 - pr * a.hr + EPC * la) * a.wc + (C0 - pc * a.wc) + EPC * lb;
+#pragma unroll
+  for (int i = 0; i < EPC; ++i) {
+    ev o;
+#pragma unroll
+    for (int j = 0; j < EPC; ++j) o[j] = in[j][i];
+    st<true>(reinterpret_cast<u32x4*>(dst + i * a.wc), __builtin_bit_cast(u32x4, o));
+  }
+}
+
 // Any shape: one element per thread, src holds X^T.
 template <typename E>
 __global__ void __launch_bounds__(256) pack_trans_scalar_kernel(TransArgs a, int64_t rows,
@@ -193,14 +238,23 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 template <typename U>
 void copy_launch(dim3 grid, const PackArgs& a, bool unpack, hipStream_t stream) {
   if (unpack)
-    hipLaunchKernelGGL((copy_kernel<U, true, false>), grid, dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((copy_kernel<U, true, false, false>), grid, dim3(256), 0, stream, a);
   else
-    hipLaunchKernelGGL((copy_kernel<U, false, false>), grid, dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((copy_kernel<U, false, false, false>), grid, dim3(256), 0, stream, a);
 }
 
+// path 2: register blocks, 1: LDS tiles, 0: one element per thread.
 template <typename E>
-void trans_launch(const Layout& L, const TransArgs& a, bool tiled, hipStream_t stream) {
-  if (tiled) {
+void trans_launch(const Layout& L, const TransArgs& a, int path, bool ntl, hipStream_t stream) {
+  if (path == 2) {
+    constexpr int WB = 8 * 16 / (int)sizeof(E);
+    const int32_t wb_cols = (int32_t)(L.cols / WB);
+    dim3 grid((unsigned)((wb_cols + 3) / 4), (unsigned)(L.rows / WB));
+    if (ntl)
+      hipLaunchKernelGGL((pack_trans_reg_kernel<E, true>), grid, dim3(256), 0, stream, a, wb_cols);
+    else
+      hipLaunchKernelGGL((pack_trans_reg_kernel<E, false>), grid, dim3(256), 0, stream, a, wb_cols);
+  } else if (path == 1) {
     dim3 grid((unsigned)(L.cols / 64), (unsigned)(L.rows / 64));
     hipLaunchKernelGGL((pack_trans_kernel<E>), grid, dim3(256), 0, stream, a);
   } else {
@@ -236,14 +290,15 @@ hipError_t launch_copy(const Plan& p, int op, const void* rowmajor, int64_t ld, 
   a.units_per_row = make_div((uint32_t)(row_bytes / unit));
   dim3 grid(grid_x_for(a.units_per_block, 4), (unsigned)(L.grid_r * L.grid_c));
   if (vec) {
-    if (L.rows * L.cols * e > kInfinityCacheBytes) {
-      if (unpack)
-        hipLaunchKernelGGL((copy_kernel<u32x4, true, true>), grid, dim3(256), 0, stream, a);
-      else
-        hipLaunchKernelGGL((copy_kernel<u32x4, false, true>), grid, dim3(256), 0, stream, a);
-    } else {
-      copy_launch<u32x4>(grid, a, unpack, stream);
-    }
+    const bool big = L.rows * L.cols * e > kInfinityCacheBytes;
+    if (unpack && big)
+      hipLaunchKernelGGL((copy_kernel<u32x4, true, true, true>), grid, dim3(256), 0, stream, a);
+    else if (unpack)
+      hipLaunchKernelGGL((copy_kernel<u32x4, true, false, false>), grid, dim3(256), 0, stream, a);
+    else if (big)
+      hipLaunchKernelGGL((copy_kernel<u32x4, false, true, true>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((copy_kernel<u32x4, false, false, false>), grid, dim3(256), 0, stream, a);
   } else if (e == 1) {
     copy_launch<uint8_t>(grid, a, unpack, stream);
   } else if (e == 2) {
@@ -266,15 +321,21 @@ hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld,
   a.hr = L.block_rows;
   a.wc = L.block_cols;
   a.grid_c = (int32_t)L.grid_c;
-  const bool tiled = L.block_rows % 64 == 0 && L.block_cols % 64 == 0 && (ld * e) % 16 == 0 &&
-                     aligned16(src) && aligned16(dst) && L.strip_stride_bytes % 16 == 0 &&
-                     L.rows / 64 <= 65535;
+  const bool vec = (ld * e) % 16 == 0 && aligned16(src) && aligned16(dst) &&
+                   L.strip_stride_bytes % 16 == 0;
+  const int64_t wb = 8 * 16 / e;      // block edge of the register-transpose kernel
+  int path = 0;
+  if (vec && L.block_rows % wb == 0 && L.block_cols % wb == 0 && L.rows / wb <= 65535)
+    path = 2;
+  else if (vec && L.block_rows % 64 == 0 && L.block_cols % 64 == 0 && L.rows / 64 <= 65535)
+    path = 1;
+  const bool ntl = L.rows * L.cols * e > kInfinityCacheBytes;
   if (e == 1)
-    trans_launch<uint8_t>(L, a, tiled, stream);
+    trans_launch<uint8_t>(L, a, path, ntl, stream);
   else if (e == 2)
-    trans_launch<uint16_t>(L, a, tiled, stream);
+    trans_launch<uint16_t>(L, a, path, ntl, stream);
   else
-    trans_launch<uint32_t>(L, a, tiled, stream);
+    trans_launch<uint32_t>(L, a, path, ntl, stream);
   return hipGetLastError();
 }
 

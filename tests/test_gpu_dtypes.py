@@ -56,6 +56,10 @@ CASES = [
     (384, 768, 201, 3, 1, 2048, "C", 0, 2, 4, 1),        # fp32 C, per-element path
     (1024, 2048, 512, 8, 2, 4096, "C", 0, 2, 4, 0),      # fp32 C, 8 chiplets
     (256, 1024, 512, 8, 1, 4096, "B", 0, 1, 4, 0),       # fp8 B, 1 x 8
+    (256, 256, 1280, 2, 1, 4096, "A", 1, 1, 2, 16),      # fp8 transpose, register blocks:
+                                                          # 10 blocks per row, 4 per workgroup
+    (256, 512, 256, 4, 2, 4096, "B", 1, 4, 4, 4),        # fp32 A/B plan, transpose (32x32 blocks)
+    (512, 256, 192, 4, 4, 4096, "A", 1, 4, 4, 0),        # fp32 transpose, 6 blocks per strip row
 ]
 
 

@@ -97,6 +97,9 @@ def test_pack_llama_operands_full_size(gemm, tensor, trans, op, grid):
     (256, 256, 512, 1, 1, 4096, "A", 1, 0),                 # single chiplet
     (1024, 256, 320, 8, 8, 4096, "B", 0, 0),                # 8x1 grid: K split in 40-row blocks
     (256, 1024, 512, 8, 1, 4096, "A", 1, 16),               # 1x8, transposed, wide ld
+    (256, 256, 640, 2, 1, 4096, "A", 1, 8),                 # transposed: 10 register blocks per
+                                                            # row, the last workgroup half idle
+    (1024, 256, 2048, 8, 8, 4096, "B", 1, 0),               # transposed, 8x1: 256-row blocks
 ])
 def test_pack_unpack_edge_cases(M, N, K, G, Gr, P, op, trans, ld_extra):
     R, Cc = OL.operand_shape(op, M, N, K)
