@@ -32,18 +32,23 @@ PEAK_BF16_TFLOPS = 2516.6        # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense)
 PEAK_FP8_TFLOPS = 5033.2         # 256 CU x 8192 FLOP/clk x 2.4 GHz (dense fp8)
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_llama_fwd_traffic.json")
-GEMM_SRC = os.path.join(ROOT, "paper_2606_11718_amd", "csrc", "kernels", "gemm.hip")
+CSRC = os.path.join(ROOT, "paper_2606_11718_amd", "csrc")
+# the sources that fix the GEMM's memory traffic: the kernels, the
+# workgroup -> tile map and the plan that picks tile shape and raster
+GEMM_SRCS = tuple(os.path.join(CSRC, f) for f in ("kernels/gemm.hip", "host/tile_map.hpp", "host/plan.cpp"))
 
 
-def kernel_hash(src: str = GEMM_SRC) -> str:
-    """Hash of the GEMM source with comments and whitespace removed, so that
+def kernel_hash(srcs=GEMM_SRCS) -> str:
+    """Hash of the GEMM sources with comments and whitespace removed, so that
     only a change to the code itself retires the committed counters."""
     import re
-    text = open(src, encoding="utf-8").read()
-    text = re.sub(r"//[^\n]*", "", text)
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    text = "".join(text.split())
-    return hashlib.sha256(text.encode()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for src in srcs:
+        text = open(src, encoding="utf-8").read()
+        text = re.sub(r"//[^\n]*", "", text)
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        h.update("".join(text.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(launch_flops_unused=None):
@@ -151,23 +156,38 @@ def compare_layouts(reps: int):
     """Per-launch time of the same GEMM kernel under three operand layouts /
     tile maps on the Llama FFN forward shapes: CCL operands with the
     XCD-aware map (ccl_gemm), row-major operands with native dispatch, and
-    row-major operands with the XCD-aware map (ccl_gemm_rowmajor)."""
+    row-major operands with the XCD-aware map (ccl_gemm_rowmajor). The
+    XCD-aware map runs at both raster group heights (4 and 8 tile rows), so
+    each layout can be compared at its best; `plan_group_m` is the height
+    the plan picks by itself."""
     import numpy as np
     import torch
     from paper_2606_11718_amd import ccl
 
     out = {}
     for name, (M, N, K) in (("llama_up", (8192, 28672, 8192)), ("llama_down", (8192, 8192, 28672))):
-        plan = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+        plans = {}
+        for gm in (4, 8):
+            old = os.environ.get("CCL_GEMM_GROUP_M")
+            os.environ["CCL_GEMM_GROUP_M"] = str(gm)
+            try:
+                plans[gm] = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+            finally:
+                if old is None:
+                    os.environ.pop("CCL_GEMM_GROUP_M", None)
+                else:
+                    os.environ["CCL_GEMM_GROUP_M"] = old
         g = torch.Generator(device="cuda").manual_seed(7)
         A = (torch.randn(M * K, device="cuda", generator=g)).to(torch.bfloat16)
         B = (torch.randn(K * N, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
         C = torch.empty(M * N, device="cuda", dtype=torch.bfloat16)
         st = torch.cuda.current_stream()
         variants = {
-            "ccl_remap": lambda: ccl.ccl_gemm(plan, A, B, C, st),
-            "rowmajor_native": lambda: ccl.ccl_gemm_rowmajor(plan, A, B, C, 0, st),
-            "rowmajor_remap": lambda: ccl.ccl_gemm_rowmajor(plan, A, B, C, 1, st),
+            "ccl_remap_g4": lambda: ccl.ccl_gemm(plans[4], A, B, C, st),
+            "ccl_remap_g8": lambda: ccl.ccl_gemm(plans[8], A, B, C, st),
+            "rowmajor_native": lambda: ccl.ccl_gemm_rowmajor(plans[4], A, B, C, 0, st),
+            "rowmajor_remap_g4": lambda: ccl.ccl_gemm_rowmajor(plans[4], A, B, C, 1, st),
+            "rowmajor_remap_g8": lambda: ccl.ccl_gemm_rowmajor(plans[8], A, B, C, 1, st),
         }
         res = {}
         for vname, fn in variants.items():
@@ -184,6 +204,9 @@ def compare_layouts(reps: int):
             torch.cuda.synchronize()
             ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
             res[vname] = {"ms": round(ms, 4), "tflops": round(2 * M * N * K / ms / 1e9, 1)}
+        default = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+        res["plan_group_m"] = next(gm for gm in (4, 8) if all(
+            ccl.ccl_debug_tile_of_wg(default, w) == ccl.ccl_debug_tile_of_wg(plans[gm], w) for w in range(0, 4096, 7)))
         out[name] = res
     return out
 
@@ -274,6 +297,58 @@ def fp8_gemms(reps: int):
     return out
 
 
+def pack_hbm(reps: int):
+    """HBM rate of the pack kernels on the Llama-3.1-70B operands, each
+    timed alone: the row-major packs of the forward pass (X, W_up), the
+    stored-transpose packs of the backward pass (X^T as A of dW_up = X^T dY,
+    W_up^T as B of dX = dY W_up^T, both on the 1x8 grid) and the unpack of
+    Y. Tensors smaller than the 256 MB Infinity Cache rotate over buffer
+    sets of more than 1 GB in total, so every launch reads and writes HBM.
+    Bytes = read + write of the logical tensor (padding is never written)."""
+    import torch
+    from paper_2606_11718_amd import ccl
+
+    cases = [
+        # name, plan (M, N, K, Gr), operand, stored rows x cols, transposed, unpack
+        ("pack_X", (8192, 28672, 8192, 2), ccl.CCL_A, (8192, 8192), 0, False),
+        ("pack_W_up", (8192, 28672, 8192, 2), ccl.CCL_B, (8192, 28672), 0, False),
+        ("pack_trans_X_T", (8192, 28672, 8192, 1), ccl.CCL_A, (8192, 8192), 1, False),
+        ("pack_trans_W_up_T", (8192, 8192, 28672, 1), ccl.CCL_B, (8192, 28672), 1, False),
+        ("unpack_Y", (8192, 8192, 28672, 2), ccl.CCL_C, (8192, 8192), 0, True),
+    ]
+    st = torch.cuda.current_stream()
+    out = {}
+    for name, (M, N, K, gr), op, (sr, sc), trans, unpack in cases:
+        plan = ccl.ccl_plan(M, N, K, 8, gr, 4096)
+        lay = ccl.ccl_plan_layout(plan, op)
+        nbytes = sr * sc * 2
+        sets = 1 if nbytes > (256 << 20) else (1 << 30) // nbytes + 1
+        rm = [torch.empty(sr * sc, dtype=torch.int16, device="cuda") for _ in range(sets)]
+        cc = [torch.empty(lay.total_bytes // 2, dtype=torch.int16, device="cuda") for _ in range(sets)]
+        if unpack:
+            calls = [(lambda r=r, c=c: ccl.ccl_unpack(plan, op, c, r, sc, st)) for r, c in zip(rm, cc)]
+        else:
+            calls = [(lambda r=r, c=c: ccl.ccl_pack(plan, op, r, sc, trans, c, st)) for r, c in zip(rm, cc)]
+        for c in calls[:3]:
+            c()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+        n = max(reps, 2 * sets)
+        e0.record(st)
+        for i in range(n):
+            calls[i % sets]()
+        e1.record(st)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        gbs = 2 * nbytes / (ms * 1e-3) / 1e9
+        out[name] = {"MB": round(nbytes / 1e6, 1), "buffer_sets": sets, "ms": round(ms, 4),
+                     "GBs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        del rm, cc, calls
+        torch.cuda.empty_cache()
+    out["peak"] = PEAK_HBM_GBS
+    return out
+
+
 def workload_gemms(reps: int):
     """Per-launch time of ccl_gemm on every workload GEMM shape (bf16, random
     operands already in CCL), at the grid the parity tests use: the small
@@ -342,6 +417,8 @@ def main():
                     help="only time the fp8 GEMMs, print one JSON line")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip timing the GEMM of every workload shape")
+    ap.add_argument("--no-pack-hbm", action="store_true",
+                    help="skip timing the pack kernels alone on rotating buffers")
     ap.add_argument("--clock-seconds", type=float, default=4.0,
                     help="sustained run after the timed steps that samples clock/power (0: off)")
     args = ap.parse_args()
@@ -498,6 +575,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_fp8:
         out["fp8_gemm"] = fp8_gemms(args.reps)
+    if not args.no_pack_hbm:
+        out["pack_hbm"] = pack_hbm(args.reps)
     if not args.no_workloads:
         out["workload_gemms"] = workload_gemms(args.reps)
     if not args.no_cpu_baseline:

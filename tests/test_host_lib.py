@@ -183,6 +183,33 @@ def test_workgroup_tile_map_covers_each_tile_once_on_owner_xcd(M, N, K, G, Gr):
     assert ccl.ccl_debug_tile_of_wg(p, wgs)[1] == -1
 
 
+@pytest.mark.parametrize("M,N,K,G,Gr", [(8192, 28672, 8192, 8, 2), (8192, 8192, 28672, 8, 2),
+                                        (8192, 28672, 8192, 8, 1), (8192, 8192, 28672, 8, 1)])
+def test_resident_tiles_share_twelve_panels(M, N, K, G, Gr):
+    """Each XCD runs 32 of its 256x256 tiles at once (one workgroup per CU,
+    in slot order). Where the partition's tile columns allow it (a multiple
+    of 8, or of 4 with a multiple of 8 tile rows), every such wave must cover
+    a 4x8 or 8x4 block of tiles: 12 distinct A row panels plus B column
+    panels, never a wave split over two raster groups. Otherwise (14 tile
+    columns for dW_up on 1x8) a straddling wave touches at most 16."""
+    p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
+    tm_, tn_, wgs = ccl.ccl_debug_gemm_config(p)
+    assert (tm_, tn_) == (256, 256)
+    tiles_m, tiles_n = M // Gr // 256, N // (G // Gr) // 256
+    exact = tiles_n % 8 == 0 or (tiles_n % 4 == 0 and tiles_m % 8 == 0)
+    slots = wgs // 8
+    for xcd in range(8):
+        tiles = [ccl.ccl_debug_tile_of_wg(p, xcd + 8 * s)[1:] for s in range(slots)]
+        for w in range(0, slots, 32):
+            wave = [t for t in tiles[w:w + 32] if t[0] >= 0]
+            rows = {t[0] for t in wave}
+            cols = {t[1] for t in wave}
+            if len(wave) == 32 and exact:
+                assert len(rows) + len(cols) == 12, (xcd, w, sorted(rows), sorted(cols))
+            else:
+                assert len(rows) + len(cols) <= (12 if exact else 16)
+
+
 def test_gemm_config_tiles_nest_in_partitions():
     for (M, N, K, G, Gr) in TILE_CASES:
         p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
