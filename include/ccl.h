@@ -30,8 +30,9 @@
  *     nothing is launched; ccl_last_error() gives a per-thread message.
  *   - Tuning overrides, read when a plan is made: CCL_GEMM_TILE=RxC (kernel
  *     tile 256x256, 256x128, 128x256 or 128x128), CCL_GEMM_WAVES=4|8 (waves
- *     of a 256x256 tile) and CCL_GEMM_GROUP_M=n (rows of the tile raster
- *     group). Unset, the plan chooses.
+ *     per workgroup; 8, the default, exists for every bf16 tile and for fp8
+ *     256x256 tiles) and CCL_GEMM_GROUP_M=n (rows of the tile raster group).
+ *     Unset, the plan chooses.
  *
  * CCL layout of an operand X (R x Cc) under a Gr x Gc grid (the same grid
  * is laid over each operand's own rows and columns: A is split along K by

@@ -45,7 +45,7 @@ struct GemmConfig {
   int64_t tiles_per_xcd = 0;        // ceil(tiles per partition / xcd_per_chiplet)
   int64_t workgroups = 0;           // 8 * tiles_per_xcd
   int group_m = 0;                  // raster group height (tiles) inside a partition
-  int waves = 4;                    // waves per workgroup (8 only for 256x256)
+  int waves = 4;                    // waves per workgroup (4 or 8)
   bool supported = false;           // whether ccl_gemm can run this plan
   std::string why_unsupported;
 };

@@ -1173,6 +1173,9 @@ static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t
 #define CCL_REDUCE_MD(BM_, BN_, WGN_) \
   do { if (md == 16) CCL_REDUCE(BM_, BN_, WGN_, 16); else CCL_REDUCE(BM_, BN_, WGN_, 32); } while (0)
   if (g.tile_m == 256 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE_MD(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 128 && g.waves == 8) CCL_REDUCE_MD(256, 128, 4);
+  else if (g.tile_m == 128 && g.tile_n == 256 && g.waves == 8) CCL_REDUCE_MD(128, 256, 4);
+  else if (g.tile_m == 128 && g.tile_n == 128 && g.waves == 8) CCL_REDUCE_MD(128, 128, 4);
   else if (g.tile_m == 256 && g.tile_n == 256) CCL_REDUCE_MD(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128) CCL_REDUCE_MD(256, 128, 2);
   else if (g.tile_m == 128 && g.tile_n == 256) CCL_REDUCE_MD(128, 256, 2);
@@ -1257,6 +1260,12 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                      stream, gp)
   if (g.tile_m == 256 && g.tile_n == 256 && waves == 8)
     CCL_LAUNCH(256, 256, 4);
+  else if (g.tile_m == 256 && g.tile_n == 128 && waves == 8)
+    CCL_LAUNCH(256, 128, 4);
+  else if (g.tile_m == 128 && g.tile_n == 256 && waves == 8)
+    CCL_LAUNCH(128, 256, 4);
+  else if (g.tile_m == 128 && g.tile_n == 128 && waves == 8)
+    CCL_LAUNCH(128, 128, 4);
   else if (g.tile_m == 256 && g.tile_n == 256)
     CCL_LAUNCH(256, 256, 2);
   else if (g.tile_m == 256 && g.tile_n == 128)

@@ -82,7 +82,8 @@ def test_qwen_backward_grids_are_the_automatic_choice():
 
 
 @pytest.mark.parametrize("tile,waves", [("256x256", 8), ("256x128", 4), ("128x256", 4),
-                                        ("128x128", 4)])
+                                        ("128x128", 4), ("256x128", 8), ("128x256", 8),
+                                        ("128x128", 8)])
 @pytest.mark.parametrize("M,N,K,G,Gr", [(2048, 2048, 1024, 8, 2),      # 2x4 grid, 32 K steps
                                         (1024, 1024, 1056, 1, 1)])     # 33 K steps: ragged stage ring
 def test_gemm_every_kernel_variant(tile, waves, M, N, K, G, Gr):

@@ -100,6 +100,23 @@ def test_splitk_bf16_matches_oracle(M, N, K, G, Gr, ta, tb, splits, ranges, c):
         assert OG.within_tolerance(err)
 
 
+@pytest.mark.parametrize("tile,waves,M,N,K,G,Gr,splits", [
+    ("128x128", 8, 768, 2048, 4096, 8, 1, 2),   # Qwen3 dW_down shape, 8 waves of 64x32
+    ("256x128", 8, 2048, 1536, 4096, 8, 2, 3),  # 8 waves of 128x32
+    ("128x256", 8, 1024, 2048, 2048, 8, 2, 4),
+])
+def test_splitk_eight_wave_tiles(tile, waves, M, N, K, G, Gr, splits, monkeypatch):
+    monkeypatch.setenv("CCL_GEMM_TILE", tile)
+    monkeypatch.setenv("CCL_GEMM_WAVES", str(waves))
+    A = _draw(BF16, 9300 + M + K, M, K)
+    B = _draw(BF16, 9400 + N + K, K, N, "normal", 0.05)
+    C, got = run_splitk(A, B, M, N, K, G, Gr, BF16, FP32, splits)
+    assert got == splits
+    err = OG.errors(C, OG.gemm_fp64(A, B))
+    print(tile, waves, "errors", err, flush=True)
+    assert err["rel_fro"] <= 1e-4
+
+
 @pytest.mark.parametrize("M,N,K,G,Gr,splits", [
     (768, 2048, 4096, 8, 1, 4),
     (256, 512, 320, 1, 1, 4),                  # 5 fp8 K steps: ranges 2, 2, 1
