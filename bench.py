@@ -146,10 +146,43 @@ def cpu_baseline(target_s: float):
     rows = max(128, (rows // 64) * 64)
     t = run(rows)
     flops = 2.0 * rows * (g_up.N * g_up.K + g_dn.N * g_dn.K)
+    blas = [f"{i.get('internal_api')} {i.get('version')} ({i.get('num_threads')} threads)"
+            for i in info if i.get("user_api") == "blas"]
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"fp64 oracle GEMMs (numpy BLAS) of the step, first {rows} of 8192 token rows "
-                      f"of X W_up and H W_down: {flops / 1e12:.3f} TFLOP in {t:.2f} s"}
+                      f"of X W_up and H W_down: {flops / 1e12:.3f} TFLOP in {t:.2f} s",
+            "cpu_model": _cpu_model(), "host_cpus": len(os.sched_getaffinity(0)), "blas": blas,
+            "other_oracle_parts": _oracle_other_parts(ops[0][0])}
+
+
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo", encoding="utf-8"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_other_parts(X_bits):
+    """The oracle's CCL pack of X (numpy reshape/transpose, 8192 x 8192 bf16,
+    2 x 4 grid) and its remote-byte model under each placement on the Qwen3
+    gate/up shape (4096 x 1536 x 2048, 2 x 4 grid, 4 KB pages), each timed
+    once on the host."""
+    from oracle import layout as OL
+    from oracle import traffic as OT
+    t0 = time.perf_counter()
+    OL.pack_reshape(X_bits, 2, 4, 4096)
+    t_pack = time.perf_counter() - t0
+    model = {}
+    for name, pl in (("rr", OT.RR), ("coarse", OT.COARSE), ("ccl", OT.CCL)):
+        t0 = time.perf_counter()
+        OT.remote_bytes(4096, 1536, 2048, 2, 4, 4096, pl)
+        model[name] = round(time.perf_counter() - t0, 3)
+    return {"pack_X_GBs": round(2 * X_bits.nbytes / t_pack / 1e9, 2),
+            "byte_model_qwen_gate_up_s": model}
 
 
 def compare_layouts(reps: int):
@@ -558,7 +591,9 @@ def main():
                      "traffic": traffic,
                      "kernel": "gemm_kernel<256,256,%d waves> (up and down launches)" % (
                          8 if ccl.ccl_debug_gemm_config(plan_up)[:2] == (256, 256) else 4),
-                     "avg_launch_ms": round(gemm_ms, 4)},
+                     "avg_launch_ms": round(gemm_ms, 4),
+                     "launch_ms": {g: {"mean": round(avg[g], 4), "median": round(float(np.median(per[g])), 4),
+                                       "min": round(float(np.min(per[g])), 4)} for g in ("gemm_up", "gemm_down")}},
         "kernels_ms": {k: round(v, 4) for k, v in avg.items()},
         "copy_roofline": {"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
                           "pack_x": round(copy_bytes / (avg["pack_x"] * 1e-3) / 1e9, 1),
