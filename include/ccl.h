@@ -269,10 +269,14 @@ typedef struct {
   int32_t line_bytes; /* power of two, 16 .. page_bytes */
   int32_t slots;      /* tiles a chiplet runs at once (its CTA concurrency), >= 1 */
   int32_t k_step;     /* K elements every resident tile reads per step, >= 1 */
-  int32_t traversal;  /* order of a chiplet's tiles: 0 tile rows outer, 1 tile columns outer */
+  int32_t traversal;  /* order of a chiplet's tiles: 0 tile rows outer, 1 tile columns outer,
+                         2 grouped raster (the partition's tile rows in groups of group_rows,
+                         the last one possibly shorter; each group walked column by column
+                         down its rows, as the GEMM kernel's workgroup map does) */
   int32_t threads;    /* host threads (capped at the core count); 0 = one per chiplet,
                          up to the core count. Each thread holds one chiplet's tags:
                          l2_bytes / line_bytes * 8 bytes of host memory. */
+  int32_t group_rows; /* traversal 2: tile rows per group, >= 1; ignored otherwise */
 } ccl_l2_config;
 
 /* Result of ccl_remote_bytes_l2. Index [0]=A, [1]=B, [2]=C. */

@@ -137,8 +137,11 @@ def _slice_lines(op, rows, cols, M, N, K, Gr, Gc, P, placement, trans, e, line):
     return [int(x) for x in lines], [int(h) for h in homes]
 
 
-def partition_tiles(p, M, N, Gr, Gc, traversal):
-    """Tiles (ti, tj) of partition p in traversal order."""
+def partition_tiles(p, M, N, Gr, Gc, traversal, group_rows=0):
+    """Tiles (ti, tj) of partition p in traversal order: "row" (tile rows
+    outer), "col" (tile columns outer) or "group" (the partition's tile rows
+    cut into groups of group_rows, the last one shorter if needed; the
+    groups in order, each walked column by column down its rows)."""
     TR, TC = M // (Gr * TILE), N // (Gc * TILE)
     pr, pc = p // Gc, p % Gc
     rows = range(pr * TR, (pr + 1) * TR)
@@ -147,12 +150,20 @@ def partition_tiles(p, M, N, Gr, Gc, traversal):
         return [(ti, tj) for ti in rows for tj in cols]
     if traversal == "col":
         return [(ti, tj) for tj in cols for ti in rows]
+    if traversal == "group":
+        if group_rows < 1:
+            raise ValueError(group_rows)
+        out = []
+        for g0 in range(0, TR, group_rows):
+            grp = rows[g0:g0 + group_rows]
+            out += [(ti, tj) for tj in cols for ti in grp]
+        return out
     raise ValueError(traversal)
 
 
 def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
              l2_bytes, slots, ways=16, line=128, k_step=64, traversal="row", e=2,
-             c_read=False):
+             c_read=False, group_rows=0):
     """Remote-HBM traffic of C = A B with a private L2 per chiplet.
 
     Returns a dict of Python ints:
@@ -173,7 +184,7 @@ def simulate(M, N, K, Gr, Gc, P, placement, trans_a=0, trans_b=0, *,
     trans = {"A": trans_a, "B": trans_b, "C": 0}
     for p in range(G):
         cache = LRUCache(l2_bytes, ways, line)
-        tiles = partition_tiles(p, M, N, Gr, Gc, traversal)
+        tiles = partition_tiles(p, M, N, Gr, Gc, traversal, group_rows)
         for w0 in range(0, len(tiles), slots):
             wave = tiles[w0:w0 + slots]
             for s in range(nk):

@@ -51,7 +51,7 @@ class _Traffic(ctypes.Structure):
 class _L2Config(ctypes.Structure):
     _fields_ = [("l2_bytes", ctypes.c_int64), ("ways", ctypes.c_int32), ("line_bytes", ctypes.c_int32),
                 ("slots", ctypes.c_int32), ("k_step", ctypes.c_int32), ("traversal", ctypes.c_int32),
-                ("threads", ctypes.c_int32)]
+                ("threads", ctypes.c_int32), ("group_rows", ctypes.c_int32)]
 
 
 class _L2Traffic(ctypes.Structure):
@@ -246,8 +246,8 @@ def ccl_remote_bytes(plan: Plan, placement: int, flags: int) -> dict:
 
 def ccl_remote_bytes_l2(plan: Plan, placement: int, flags: int, *, l2_bytes: int,
                         slots: int, ways: int = 16, line_bytes: int = 128, k_step: int = 64,
-                        traversal: int = 0, threads: int = 0) -> dict:
-    cfg = _L2Config(l2_bytes, ways, line_bytes, slots, k_step, traversal, threads)
+                        traversal: int = 0, threads: int = 0, group_rows: int = 0) -> dict:
+    cfg = _L2Config(l2_bytes, ways, line_bytes, slots, k_step, traversal, threads, group_rows)
     t = _L2Traffic()
     _check(library().ccl_remote_bytes_l2(plan, placement, flags, ctypes.byref(cfg),
                                          ctypes.byref(t)))

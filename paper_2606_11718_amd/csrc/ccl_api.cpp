@@ -323,6 +323,7 @@ ccl_status ccl_remote_bytes_l2(ccl_plan_t plan, ccl_placement placement, int fla
   c.slots = config->slots;
   c.k_step = config->k_step;
   c.traversal = config->traversal;
+  c.group_rows = config->group_rows;
   c.threads = config->threads;
   std::string why = ccl::check_l2_config(c);
   if (why.empty() && c.line > plan->plan.page) why = "line_bytes must not exceed the page size";

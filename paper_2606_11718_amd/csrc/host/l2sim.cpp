@@ -177,9 +177,18 @@ ChipletCount simulate_chiplet(const Plan& p, int chip, const Stored* st, const L
     if (c.traversal == 0) {
       *ti = pr * TR + t / TC;
       *tj = pc * TC + t % TC;
-    } else {
+    } else if (c.traversal == 1) {
       *tj = pc * TC + t / TR;
       *ti = pr * TR + t % TR;
+    } else {
+      // groups of group_rows tile rows (the last one may be shorter), each
+      // walked column by column down its rows
+      const int64_t per_group = int64_t(c.group_rows) * TC;
+      const int64_t first = (t / per_group) * c.group_rows;
+      const int64_t gm = std::min<int64_t>(c.group_rows, TR - first);
+      const int64_t w = t - (t / per_group) * per_group;
+      *ti = pr * TR + first + w % gm;
+      *tj = pc * TC + w / gm;
     }
   };
   const int64_t T = kModelTile;
@@ -226,7 +235,9 @@ std::string check_l2_config(const L2Config& c) {
   if (c.ways < 1) return "ways must be >= 1";
   if (c.slots < 1) return "slots must be >= 1";
   if (c.k_step < 1) return "k_step must be >= 1";
-  if (c.traversal != 0 && c.traversal != 1) return "traversal must be 0 (rows) or 1 (columns)";
+  if (c.traversal < 0 || c.traversal > 2)
+    return "traversal must be 0 (rows), 1 (columns) or 2 (grouped raster)";
+  if (c.traversal == 2 && c.group_rows < 1) return "group_rows must be >= 1 for traversal 2";
   if (c.threads < 0) return "threads must be >= 0";
   if (c.l2_bytes < 0) return "l2_bytes must be >= 0";
   if (c.l2_bytes > 0) {

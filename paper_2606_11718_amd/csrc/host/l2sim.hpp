@@ -15,7 +15,8 @@ struct L2Config {
   int line = 128;         // bytes, power of two
   int slots = 32;         // tiles resident per chiplet at once
   int k_step = 64;        // K elements each resident tile reads per step
-  int traversal = 0;      // 0: tile rows outer, 1: tile columns outer
+  int traversal = 0;      // 0: tile rows outer, 1: tile columns outer, 2: grouped raster
+  int group_rows = 0;     // traversal 2: tile rows per group (each group walked column by column)
   int threads = 0;        // host threads (0: one per chiplet, up to the core count)
 };
 

@@ -21,7 +21,7 @@ from paper_2606_11718_amd import ccl
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GOLDEN = os.path.join(ROOT, "tests", "golden", "l2_golden.json")
 PLACE = {"rr": ccl.CCL_PLACE_RR, "coarse": ccl.CCL_PLACE_COARSE, "ccl": ccl.CCL_PLACE_CCL}
-TRAV = {"row": 0, "col": 1}
+TRAV = {"row": 0, "col": 1, "group": 2}
 
 
 def _both(M, N, K, G, Gr, P, placement, ta, tb, c_read=False, **cfg):
@@ -30,10 +30,12 @@ def _both(M, N, K, G, Gr, P, placement, ta, tb, c_read=False, **cfg):
     lib = ccl.ccl_remote_bytes_l2(plan, PLACE[placement], flags,
                                   l2_bytes=cfg["l2_bytes"], slots=cfg["slots"], ways=cfg["ways"],
                                   line_bytes=cfg.get("line", 128), k_step=cfg["k_step"],
-                                  traversal=TRAV[cfg["traversal"]])
+                                  traversal=TRAV[cfg["traversal"]],
+                                  group_rows=cfg.get("group_rows", 0))
     ora = L.simulate(M, N, K, Gr, G // Gr, P, placement, ta, tb, l2_bytes=cfg["l2_bytes"],
                      slots=cfg["slots"], ways=cfg["ways"], line=cfg.get("line", 128),
-                     k_step=cfg["k_step"], traversal=cfg["traversal"], c_read=c_read)
+                     k_step=cfg["k_step"], traversal=cfg["traversal"], c_read=c_read,
+                     group_rows=cfg.get("group_rows", 0))
     return lib, ora
 
 
@@ -52,6 +54,8 @@ CFGS = [
     dict(l2_bytes=8 * 4 * 128, ways=4, slots=3, k_step=128, traversal="col"),
     dict(l2_bytes=64 * 8 * 128, ways=8, slots=4, k_step=32, traversal="row"),
     dict(l2_bytes=1 * 256 * 128, ways=256, slots=2, k_step=64, traversal="col"),   # fully associative
+    dict(l2_bytes=8 * 8 * 128, ways=8, slots=3, k_step=64, traversal="group", group_rows=1),
+    dict(l2_bytes=16 * 4 * 128, ways=4, slots=2, k_step=128, traversal="group", group_rows=3),
 ]
 
 
@@ -119,6 +123,21 @@ def test_llama_full_size_properties():
     assert 0 < sum(rec["remote"]) <= floor
 
 
+@pytest.mark.parametrize("M,N,K,group_rows", [(8192, 28672, 8192, 16), (8192, 8192, 28672, 8)])
+def test_kernel_schedule_misses_reach_the_panel_floor(M, N, K, group_rows):
+    """The GEMM kernel's own schedule on MI355X, in model terms: 32 resident
+    256x256 tiles per XCD = 128 model tiles, a grouped raster of 8 (up) or 4
+    (down) kernel tile rows, K steps of 32, a 4 MB 16-way L2 of 128-byte
+    lines. With CCL operands every wave of 32 kernel tiles touches 12 panels
+    of 256 x K bf16 once: misses = 8 XCDs x waves x 12 x 256 K 2 bytes, the
+    fetch the hardware counters measure for these launches (5.64 GB)."""
+    plan = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+    r = ccl.ccl_remote_bytes_l2(plan, ccl.CCL_PLACE_CCL, 0, l2_bytes=4 << 20, slots=128, ways=16,
+                                line_bytes=128, k_step=32, traversal=2, group_rows=group_rows)
+    waves = (M // 2 // 256) * (N // 4 // 256) // 32
+    assert (r["misses"][0] + r["misses"][1]) * 128 == 8 * waves * 12 * 256 * K * 2
+
+
 @pytest.mark.parametrize("bad", [
     dict(l2_bytes=3 * 16 * 128),          # 3 sets
     dict(l2_bytes=1000),                  # not whole sets
@@ -128,7 +147,9 @@ def test_llama_full_size_properties():
     dict(line_bytes=8192),                # larger than the 4 KB page
     dict(slots=0),
     dict(k_step=0),
-    dict(traversal=2),
+    dict(traversal=3),
+    dict(traversal=2),                    # grouped raster without a group height
+    dict(traversal=2, group_rows=-1),
     dict(threads=-1),
     dict(l2_bytes=(1 << 25) * 128, ways=1),   # more than 2^24 lines
 ])

@@ -101,9 +101,9 @@ PLACEMENTS = ("rr", "coarse", "ccl")
 def test_capacity_zero_is_tile_charge(case, placement):
     M, N, K, Gr, Gc, P, ta, tb = case
     ref = T.remote_bytes(M, N, K, Gr, Gc, P, placement, ta, tb)
-    for slots, trav, ks in ((1, "row", 64), (3, "col", 128)):   # K step 128: ragged last step
+    for slots, trav, ks in ((1, "row", 64), (3, "col", 128), (2, "group", 64)):   # K step 128: ragged last step
         got = L.simulate(M, N, K, Gr, Gc, P, placement, ta, tb, l2_bytes=0, slots=slots,
-                         traversal=trav, k_step=ks)
+                         traversal=trav, k_step=ks, group_rows=1 + (M // 128) // 3)
         assert got["remote"] == ref["remote"]
         assert got["remote_per_chiplet"] == ref["remote_per_chiplet"]
         assert got["misses"] == got["accesses"]
@@ -201,6 +201,40 @@ def test_partition_tiles_order():
     # 512 x 512 output, 2 x 2 grid: partition 3 holds tiles (2..3, 2..3)
     assert L.partition_tiles(3, 512, 512, 2, 2, "row") == [(2, 2), (2, 3), (3, 2), (3, 3)]
     assert L.partition_tiles(3, 512, 512, 2, 2, "col") == [(2, 2), (3, 2), (2, 3), (3, 3)]
+
+
+def test_partition_tiles_group_order():
+    # 640 x 256 output, one partition: 5 tile rows x 2 tile columns in groups
+    # of 2 rows (the last group has 1), each group walked column by column
+    assert L.partition_tiles(0, 640, 256, 1, 1, "group", 2) == [
+        (0, 0), (1, 0), (0, 1), (1, 1), (2, 0), (3, 0), (2, 1), (3, 1), (4, 0), (4, 1)]
+    # partition 1 of a 1 x 2 grid over 640 x 512 holds tile columns 2..3
+    assert L.partition_tiles(1, 640, 512, 1, 2, "group", 4) == [
+        (0, 2), (1, 2), (2, 2), (3, 2), (0, 3), (1, 3), (2, 3), (3, 3), (4, 2), (4, 3)]
+    # one-row groups are the row order; one group of all rows is the column order
+    for p in range(4):
+        assert L.partition_tiles(p, 1024, 768, 2, 2, "group", 1) == L.partition_tiles(p, 1024, 768, 2, 2, "row")
+        assert L.partition_tiles(p, 1024, 768, 2, 2, "group", 4) == L.partition_tiles(p, 1024, 768, 2, 2, "col")
+        assert L.partition_tiles(p, 1024, 768, 2, 2, "group", 9) == L.partition_tiles(p, 1024, 768, 2, 2, "col")
+    with pytest.raises(ValueError):
+        L.partition_tiles(0, 256, 256, 1, 1, "group", 0)
+
+
+def test_order_grouped_waves_share_panels():
+    # M = N = 512, K = 64 (one K step), one chiplet, waves of 4 tiles, a
+    # fully associative LRU cache of 4 slices (512 lines; a slice is 128).
+    # Grouped (2 rows), worked through access by access:
+    #   wave 1 (0,0) (1,0) (0,1) (1,1): A0 A1 B0 B1 miss once each;
+    #   wave 2 (0,2) (1,2) (0,3) (1,3): A0 A1 hit, B2 B3 miss;
+    #   wave 3 (2,0) (3,0) (2,1) (3,1): A2 A3 B0 B1 miss;
+    #   wave 4 (2,2) (3,2) (2,3) (3,3): A2 A3 hit, B2 B3 miss.
+    # A misses 4 slices, B misses 8. Row order puts A0 and B0..B3 (5 slices)
+    # in one wave, which does not fit, so it misses more B.
+    kw = dict(l2_bytes=512 * 128, ways=512, slots=4, k_step=64)
+    grp = L.simulate(512, 512, 64, 1, 1, 4096, "rr", traversal="group", group_rows=2, **kw)
+    row = L.simulate(512, 512, 64, 1, 1, 4096, "rr", traversal="row", **kw)
+    assert grp["misses"] == [4 * 128, 8 * 128]
+    assert row["misses"][1] > grp["misses"][1]
 
 
 # ---------------------------------------------------------------------------
