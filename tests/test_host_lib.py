@@ -191,7 +191,9 @@ def test_resident_tiles_share_twelve_panels(M, N, K, G, Gr):
     of 8, or of 4 with a multiple of 8 tile rows), every such wave must cover
     a 4x8 or 8x4 block of tiles: 12 distinct A row panels plus B column
     panels, never a wave split over two raster groups. Otherwise (14 tile
-    columns for dW_up on 1x8) a straddling wave touches at most 16."""
+    columns for dW_up on 1x8) some waves straddle two groups; there the
+    plan's height is the one with the fewest panels in total
+    (test_raster_height_touches_fewest_panels)."""
     p = ccl.ccl_plan(M, N, K, G, Gr, 4096)
     tm_, tn_, wgs = ccl.ccl_debug_gemm_config(p)
     assert (tm_, tn_) == (256, 256)
@@ -204,10 +206,40 @@ def test_resident_tiles_share_twelve_panels(M, N, K, G, Gr):
             wave = [t for t in tiles[w:w + 32] if t[0] >= 0]
             rows = {t[0] for t in wave}
             cols = {t[1] for t in wave}
-            if len(wave) == 32 and exact:
+            if exact and len(wave) == 32:
                 assert len(rows) + len(cols) == 12, (xcd, w, sorted(rows), sorted(cols))
-            else:
-                assert len(rows) + len(cols) <= (12 if exact else 16)
+            elif exact:
+                assert len(rows) + len(cols) <= 12
+
+
+def _wave_panels(p):
+    """Distinct tile rows plus tile columns of every wave of 32 consecutive
+    slots on each XCD, summed (from the plan's workgroup -> tile map)."""
+    _, _, wgs = ccl.ccl_debug_gemm_config(p)
+    slots, total = wgs // 8, 0
+    for xcd in range(8):
+        tiles = [ccl.ccl_debug_tile_of_wg(p, xcd + 8 * s)[1:] for s in range(slots)]
+        for w in range(0, slots, 32):
+            wave = [t for t in tiles[w:w + 32] if t[0] >= 0]
+            total += len({t[0] for t in wave}) + len({t[1] for t in wave})
+    return total
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(8192, 28672, 8192, 8, 2), (8192, 8192, 28672, 8, 2),
+                                        (8192, 28672, 8192, 8, 1), (8192, 8192, 28672, 8, 1),
+                                        (4096, 1536, 2048, 8, 2), (2048, 4096, 1024, 4, 2)])
+def test_raster_height_touches_fewest_panels(M, N, K, G, Gr, monkeypatch):
+    """The plan's raster is at least as good as 4- and 8-row groups in
+    panels touched per wave, and it is 4 rows on a tie."""
+    chosen = _wave_panels(ccl.ccl_plan(M, N, K, G, Gr, 4096))
+    forced = {}
+    for gm in (4, 8):
+        monkeypatch.setenv("CCL_GEMM_GROUP_M", str(gm))
+        forced[gm] = _wave_panels(ccl.ccl_plan(M, N, K, G, Gr, 4096))
+    monkeypatch.delenv("CCL_GEMM_GROUP_M")
+    assert chosen == min(forced.values())
+    if forced[4] == forced[8]:
+        assert chosen == forced[4]
 
 
 def test_gemm_config_tiles_nest_in_partitions():
