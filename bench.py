@@ -185,14 +185,17 @@ def _oracle_other_parts(X_bits):
             "byte_model_qwen_gate_up_s": model}
 
 
-def compare_layouts(reps: int):
+def compare_layouts(reps: int, sustained: float = 0.0, rounds: int = 1):
     """Per-launch time of the same GEMM kernel under three operand layouts /
     tile maps on the Llama FFN forward shapes: CCL operands with the
     XCD-aware map (ccl_gemm), row-major operands with native dispatch, and
     row-major operands with the XCD-aware map (ccl_gemm_rowmajor). The
     XCD-aware map runs at both raster group heights (4 and 8 tile rows), so
     each layout can be compared at its best; `plan_group_m` is the height
-    the plan picks by itself."""
+    the plan picks by itself. With `sustained` > 0 each variant first runs
+    back to back for that many seconds, so the power-limited clock settles
+    at its own level; `rounds` > 1 alternates the variants that many times
+    and reports every round's median."""
     import numpy as np
     import torch
     from paper_2606_11718_amd import ccl
@@ -223,20 +226,30 @@ def compare_layouts(reps: int):
             "rowmajor_remap_g8": lambda: ccl.ccl_gemm_rowmajor(plans[8], A, B, C, 1, st),
         }
         res = {}
-        for vname, fn in variants.items():
-            for _ in range(3):
-                fn()
-            torch.cuda.synchronize()
-            ts = []
-            for _ in range(reps):
-                e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
-                e0.record(st)
-                fn()
-                e1.record(st)
-                ts.append((e0, e1))
-            torch.cuda.synchronize()
-            ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
-            res[vname] = {"ms": round(ms, 4), "tflops": round(2 * M * N * K / ms / 1e9, 1)}
+        for rnd in range(rounds):
+            for vname, fn in variants.items():
+                for _ in range(3):
+                    fn()
+                torch.cuda.synchronize()
+                t_end = time.time() + sustained
+                while time.time() < t_end:
+                    for _ in range(5):
+                        fn()
+                    torch.cuda.synchronize()
+                ts = []
+                for _ in range(reps):
+                    e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+                    e0.record(st)
+                    fn()
+                    e1.record(st)
+                    ts.append((e0, e1))
+                torch.cuda.synchronize()
+                ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
+                tf = round(2 * M * N * K / ms / 1e9, 1)
+                if rounds == 1:
+                    res[vname] = {"ms": round(ms, 4), "tflops": tf}
+                else:
+                    res.setdefault(vname, {"tflops_by_round": []})["tflops_by_round"].append(tf)
         default = ccl.ccl_plan(M, N, K, 8, 2, 4096)
         res["plan_group_m"] = next(gm for gm in (4, 8) if all(
             ccl.ccl_debug_tile_of_wg(default, w) == ccl.ccl_debug_tile_of_wg(plans[gm], w) for w in range(0, 4096, 7)))
@@ -445,6 +458,10 @@ def main():
     ap.add_argument("--compare-layouts", action="store_true",
                     help="only time CCL vs row-major operands and tile maps, print one JSON line")
     ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--sustained", type=float, default=0.0,
+                    help="--compare-layouts: seconds of back-to-back launches before timing each variant")
+    ap.add_argument("--rounds", type=int, default=1,
+                    help="--compare-layouts: alternate the variants this many times")
     ap.add_argument("--no-fp8", action="store_true", help="skip the fp8 GEMM timing")
     ap.add_argument("--fp8-only", action="store_true",
                     help="only time the fp8 GEMMs, print one JSON line")
@@ -471,7 +488,8 @@ def main():
     from paper_2606_11718_amd import ccl
 
     if args.compare_layouts:
-        print(json.dumps({"compare_layouts": compare_layouts(args.reps)}), flush=True)
+        print(json.dumps({"compare_layouts": compare_layouts(args.reps, args.sustained, args.rounds)}),
+              flush=True)
         return
     if args.fp8_only:
         print(json.dumps({"fp8_gemm": fp8_gemms(args.reps)}), flush=True)
