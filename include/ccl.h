@@ -160,8 +160,12 @@ ccl_status ccl_pack(ccl_plan_t plan, ccl_operand op, const void* src, int64_t ld
 
 /*
  * Inverse of ccl_pack with src_trans = 0: CCL buffer -> row-major operand
- * (rows x cols, leading dimension ld >= cols). Columns beyond cols in each
- * dst row are not written. Errors as ccl_pack.
+ * (rows x cols, leading dimension ld >= cols). This is the inverse of the
+ * Eq. 3 map (Sec. III-B: each CCL index names exactly one element of the
+ * row-major matrix of Eq. 2), used where a CCL result, e.g. the output C of
+ * Sec. III-C, is handed to code that expects row-major. src_ccl has
+ * ccl_plan_layout().total_bytes bytes; its padding is not read. Columns
+ * beyond cols in each dst row are not written. Errors as ccl_pack.
  */
 ccl_status ccl_unpack(ccl_plan_t plan, ccl_operand op, const void* src_ccl, void* dst,
                       int64_t ld, void* stream);

@@ -73,17 +73,6 @@ def gemm_scaled_fp64(A, B, C, alpha: float, beta: float) -> np.ndarray:
     return alpha * P + beta * decode(C)
 
 
-def gemm_entries(A: np.ndarray, B: np.ndarray, rows: np.ndarray, cols: np.ndarray) -> np.ndarray:
-    """C[rows[i], cols[i]] for sampled output positions, in float64.
-
-    A holds only the rows needed (indexed by rows), B is K x N (both may be
-    bf16 bits). Used where the full product is too large for the host.
-    """
-    A = decode(A)
-    B = decode(B)
-    return np.einsum("ik,ki->i", A[rows], B[:, cols])
-
-
 def errors(C_test: np.ndarray, C_ref: np.ndarray) -> dict:
     """rel_fro = ||C_test - C_ref||_F / ||C_ref||_F, max_abs, max_ref."""
     C_test = np.asarray(C_test, dtype=np.float64)
@@ -95,6 +84,43 @@ def errors(C_test: np.ndarray, C_ref: np.ndarray) -> dict:
         "max_abs": float(np.max(np.abs(d))) if d.size else 0.0,
         "max_ref": float(np.max(np.abs(C_ref))) if C_ref.size else 0.0,
     }
+
+
+class ErrorAccumulator:
+    """errors() of a matrix that arrives in row blocks.
+
+    The definition's sums of squares (of C_test - C_ref and of C_ref) and
+    its two maxima are accumulated block by block in float64, so a product
+    too large to hold twice on the host is still compared element by
+    element. result() has the keys of errors().
+    """
+
+    def __init__(self):
+        self.sq_diff = 0.0
+        self.sq_ref = 0.0
+        self.max_abs = 0.0
+        self.max_ref = 0.0
+        self.count = 0
+
+    def add(self, C_test: np.ndarray, C_ref: np.ndarray) -> None:
+        C_test = np.asarray(C_test, dtype=np.float64)
+        C_ref = np.asarray(C_ref, dtype=np.float64)
+        if C_test.shape != C_ref.shape:
+            raise ValueError("block shapes differ")
+        if C_ref.size == 0:
+            return
+        d = (C_test - C_ref).ravel()
+        r = C_ref.ravel()
+        self.sq_diff += float(np.dot(d, d))
+        self.sq_ref += float(np.dot(r, r))
+        self.max_abs = max(self.max_abs, float(np.max(np.abs(d))))
+        self.max_ref = max(self.max_ref, float(np.max(np.abs(r))))
+        self.count += C_ref.size
+
+    def result(self) -> dict:
+        d, r = self.sq_diff ** 0.5, self.sq_ref ** 0.5
+        return {"rel_fro": d / r if r > 0 else d, "max_abs": self.max_abs,
+                "max_ref": self.max_ref}
 
 
 def within_tolerance(err: dict, rel_fro_tol: float = 5e-3, max_abs_frac: float = 1e-2) -> bool:

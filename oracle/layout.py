@@ -135,22 +135,22 @@ def unpack(buf: np.ndarray, R: int, Cc: int, Pr: int, Pc: int, P: int) -> np.nda
     return buf[ccl_offset(r, c, R, Cc, Pr, Pc, P, e) // e]
 
 
+def unpack_rows(buf: np.ndarray, R: int, Cc: int, Pr: int, Pc: int, P: int,
+                r0: int, r1: int) -> np.ndarray:
+    """Rows r0 .. r1-1 of the row-major operand held in a CCL buffer: the
+    gather of unpack(), restricted to those rows."""
+    if not 0 <= r0 <= r1 <= R:
+        raise ValueError("row range outside the operand")
+    e = buf.dtype.itemsize
+    r, c = np.meshgrid(np.arange(r0, r1), np.arange(Cc), indexing="ij")
+    return buf[ccl_offset(r, c, R, Cc, Pr, Pc, P, e) // e]
+
+
 def padding_mask(R: int, Cc: int, Pr: int, Pc: int, P: int, e: int = 2) -> np.ndarray:
     """Boolean mask over the buffer's elements: True where padding."""
     n = total_bytes(R, Cc, Pr, Pc, P, e) // e
     _, _, valid = ccl_inverse(np.arange(n, dtype=np.int64) * e, R, Cc, Pr, Pc, P, e)
     return ~valid
-
-
-def operand_grid(op: str, Gr: int, Gc: int) -> tuple[int, int]:
-    """Block grid of operand op ('A', 'B' or 'C') under a Gr x Gc GEMM grid.
-
-    The same (Gr, Gc) grid is laid over each operand's own (rows, cols):
-    A (M x K) is split along K by Gc, B (K x N) along K by Gr.
-    """
-    if op not in ("A", "B", "C"):
-        raise ValueError(op)
-    return Gr, Gc
 
 
 def operand_shape(op: str, M: int, N: int, K: int) -> tuple[int, int]:

@@ -102,13 +102,16 @@ bool addressing_in_bounds(const ccl::Plan& p, const ccl::OperandAddr& a, const c
          c_end * p.lay[ccl::OP_C].elem_bytes <= c_bytes;
 }
 
-// The kernel addresses a tile's K step with 32-bit byte offsets from its
-// corner: up to 255 rows of A and one K step minus one rows of B.
+// The kernels address a tile's K steps with 32-bit byte offsets and 32-bit
+// buffer sizes from the tile corner. The widest spans any kernel builds:
+// A, 255 rows plus four bf16 K steps (256 bytes); B, 127 rows (four bf16
+// steps of the rounds path, or one 128-wide fp8 step) plus a 256-column
+// row. Both must stay below 2^31 (less a page of margin), whichever kernel
+// the plan selects.
 bool offsets_fit(const ccl::Plan& p, const ccl::OperandAddr& a, const ccl::OperandAddr& b) {
   const int64_t lim = ((int64_t)1 << 31) - 4096;
   const int64_t e = p.lay[ccl::OP_A].elem_bytes;
-  const int64_t bk = p.ab_type == ccl::DT_FP8_E4M3 ? ccl::kGemmBK8 : ccl::kGemmBK;
-  return 255 * (int64_t)a.ld * e < lim && (bk - 1) * (int64_t)b.ld * e < lim;
+  return 255 * (int64_t)a.ld * e + 256 < lim && 127 * (int64_t)b.ld * e + 256 * e < lim;
 }
 
 }  // namespace

@@ -15,7 +15,7 @@ import workloads as W
 from oracle import gemm as OG
 from oracle import layout as OL
 from paper_2606_11718_amd import ccl
-from tests.helpers import dev_full, from_dev, to_dev
+from tests.helpers import compare_in_row_blocks, dev_full, from_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -93,9 +93,9 @@ def test_alpha_one_beta_zero_equals_ccl_gemm():
     assert np.array_equal(from_dev(C1), from_dev(C2))
 
 
-def test_llama_up_scaled_sampled():
-    """alpha X W_up + beta C0 at the Llama-3.1-70B forward shape, on sampled
-    output positions (each an fp64 dot product in the oracle)."""
+def test_llama_up_scaled_full_compare():
+    """alpha X W_up + beta C0 at the Llama-3.1-70B forward shape: every
+    element against the oracle's fp64 alpha A B + beta C0, in row blocks."""
     wl, g = W.gemm_by_name("llama_up")
     X = W.draw(wl.tensors["X"])
     Wu = W.draw(wl.tensors["W_up"])
@@ -111,14 +111,13 @@ def test_llama_up_scaled_sampled():
     ccl.ccl_pack(plan, ccl.CCL_C, to_dev(C0), g.N, 0, Cc)
     ccl.ccl_gemm_scaled(plan, alpha, Ac, Bc, beta, Cc)
     cbuf = from_dev(Cc)
-    rng = np.random.default_rng(7)
-    rows = rng.integers(0, g.M, 4096)
-    cols = rng.integers(0, g.N, 4096)
-    dots = OG.gemm_entries(X[rows], Wu[:, cols], np.arange(4096), np.arange(4096))
-    ref = alpha * dots + beta * OG.decode_bf16(C0[rows, cols])
-    got = OG.decode_bf16(cbuf[OL.ccl_offset(rows, cols, g.M, g.N, gr, gc, 4096) // 2])
-    err = OG.errors(got, ref)
-    print("sampled errors", err, flush=True)
+    del Ac, Bc, Cc
+    Wu_d = OG.decode(Wu)
+    err = compare_in_row_blocks(
+        {0: (cbuf, gr, gc)}, g.M, g.N, 4096,
+        lambda r0, r1: OG.gemm_scaled_fp64(OG.decode(X[r0:r1]), Wu_d, C0[r0:r1], alpha, beta),
+        OG.decode_bf16)[0]
+    print("errors over all of C", err, flush=True)
     assert OG.within_tolerance(err)
 
 

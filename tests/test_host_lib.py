@@ -349,6 +349,14 @@ def test_size_limits_are_rejected_before_any_launch():
     assert lib.ccl_gemm(wide, 4096, 4096, 4096, None) == 3
     assert "32-bit" in lib.ccl_last_error().decode()
     assert lib.ccl_gemm_rowmajor(wide, 4096, 4096, 4096, 1, None) == 3
+    # B rows of 17.9M bf16: one K step (31 rows) spans 1.1 GB, but four steps
+    # of the rounds path (127 rows) span 4.5 GB; the same for fp8's 128-wide step
+    for ab, n in ((ccl.CCL_DT_BF16, 128 * 140000), (ccl.CCL_DT_FP8_E4M3, 128 * 140000 * 2)):
+        longb = ccl.ccl_plan_typed(128, n, 128, 1, 1, 4096, ab, ccl.CCL_DT_BF16)
+        assert lib.ccl_gemm(longb, 4096, 4096, 4096, None) == 3
+        assert "32-bit" in lib.ccl_last_error().decode()
+        assert lib.ccl_gemm_splitk(longb, 1.0, 4096, 4096, 0.0, 4096, 2, 4096, 1 << 40, None) == 3
+        assert "32-bit" in lib.ccl_last_error().decode()
     huge = ccl.ccl_plan(65536, 128, 65536, 1, 1, 4096)      # one strip of 2^32 elements
     assert lib.ccl_pack(huge, ccl.CCL_A, 4096, 65536, 0, 4096, None) == 3
     assert lib.ccl_unpack(huge, ccl.CCL_A, 4096, 4096, 65536, None) == 3

@@ -38,11 +38,9 @@ def test_entries_match_fsum_definition():
     rng = np.random.default_rng(0)
     rows = rng.integers(0, 40, 25)
     cols = rng.integers(0, 50, 25)
-    ent = O.gemm_entries(A, B, rows, cols)
-    for i, (r, c) in enumerate(zip(rows, cols)):
+    for r, c in zip(rows, cols):
         exact = math.fsum(a[r, k] * b[k, c] for k in range(300))
         assert abs(C[r, c] - exact) <= 1e-12 * (1 + abs(exact))
-        assert abs(ent[i] - exact) <= 1e-12 * (1 + abs(exact))
 
 
 def test_error_metrics_on_known_perturbation():
@@ -124,3 +122,29 @@ def test_fp8_gemm_on_integers_is_exact():
     bi = O.decode_fp8_e4m3(B).astype(np.int64)
     assert set(np.unique(ai)) <= {-1, 0, 1}
     assert np.array_equal(O.gemm_fp64(A, B), (ai @ bi).astype(np.float64))
+
+
+@pytest.mark.parametrize("block", [1, 7, 64, 200])
+def test_error_accumulator_over_row_blocks_equals_errors(block):
+    """The block-wise form gives errors()'s values for any row blocking, and
+    still sees a single planted outlier."""
+    rng = np.random.default_rng(2)
+    ref = rng.standard_normal((200, 37))
+    test = ref + 1e-4 * rng.standard_normal((200, 37))
+    test[123, 5] += 0.3
+    acc = O.ErrorAccumulator()
+    for r0 in range(0, 200, block):
+        acc.add(test[r0:r0 + block], ref[r0:r0 + block])
+    got, want = acc.result(), O.errors(test, ref)
+    assert acc.count == ref.size
+    for key in ("rel_fro", "max_abs", "max_ref"):
+        assert math.isclose(got[key], want[key], rel_tol=1e-12), key
+    assert math.isclose(got["max_abs"], abs(test[123, 5] - ref[123, 5]), rel_tol=1e-12)
+
+
+def test_error_accumulator_rejects_mismatched_blocks():
+    acc = O.ErrorAccumulator()
+    with pytest.raises(ValueError):
+        acc.add(np.zeros((2, 3)), np.zeros((3, 2)))
+    acc.add(np.zeros((0, 4)), np.zeros((0, 4)))
+    assert acc.result() == {"rel_fro": 0.0, "max_abs": 0.0, "max_ref": 0.0}

@@ -46,6 +46,43 @@ def test_pack_matches_cute_stride_view(K, N, G):
     assert np.array_equal(view, B.reshape(K, G, w))
 
 
+@pytest.mark.parametrize("K,N,G", [(4, 8, 2), (16, 64, 4), (7, 24, 3), (32, 256, 8)])
+def test_cute_index_is_eq3_and_the_stride_view(K, N, G):
+    """Sec. III-C's coordinate form (cute_index) gives Eq. 3's index for
+    every element, and it is where the CuTe stride view (realised by numpy's
+    as_strided over a packed buffer) finds B[k, n]."""
+    k, n = np.meshgrid(np.arange(K), np.arange(N), indexing="ij")
+    idx = L.cute_index(k, n, K, N, G)
+    assert np.array_equal(idx, L.eq3_index(k, n, K, N, G))
+    assert sorted(idx.ravel()) == list(range(K * N))          # a bijection onto the buffer
+    rng = np.random.default_rng(K + N)
+    B = rng.integers(0, 65535, size=(K, N), dtype=np.uint16)
+    buf = L.pack(B, 1, G, P=2)
+    assert np.array_equal(buf[idx], B)
+    w = N // G
+    view = np.lib.stride_tricks.as_strided(buf, shape=(K, G, w),
+                                           strides=(w * buf.itemsize, K * w * buf.itemsize, buf.itemsize))
+    assert np.array_equal(view[k, n // w, n % w], buf[idx])
+
+
+def test_cute_index_worked_example():
+    """The two-chiplet example of Sec. III-A: B[1, 5] with K = 4, N = 8 sits
+    at CCL index 21 (chiplet 1's strip starts at 16)."""
+    assert int(L.cute_index(1, 5, 4, 8, 2)) == 21
+
+
+@pytest.mark.parametrize("R,Cc,Pr,Pc,P", [(64, 96, 2, 3, 4096), (256, 512, 2, 4, 65536),
+                                          (48, 40, 4, 2, 256), (33, 17, 1, 1, 4096)])
+def test_unpack_rows_is_a_row_slice_of_unpack(R, Cc, Pr, Pc, P):
+    rng = np.random.default_rng(R * Cc)
+    X = rng.integers(0, 65535, size=(R, Cc), dtype=np.uint16)
+    buf = L.pack_reshape(X, Pr, Pc, P, fill=0xFFFF)
+    for r0, r1 in ((0, R), (0, 1), (R // 3, R // 2 + 1), (R - 1, R), (5, 5)):
+        assert np.array_equal(L.unpack_rows(buf, R, Cc, Pr, Pc, P, r0, r1), X[r0:r1])
+    with pytest.raises(ValueError):
+        L.unpack_rows(buf, R, Cc, Pr, Pc, P, 0, R + 1)
+
+
 def test_two_chiplet_worked_example():
     """Sec. III-A: with two chiplets row-major alternates per-chiplet slices
     every 4 elements; CCL keeps 16 elements of one chiplet together."""
