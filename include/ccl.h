@@ -235,6 +235,28 @@ ccl_status ccl_gemm_splitk(ccl_plan_t plan, float alpha, const void* A_ccl, cons
                            int64_t workspace_bytes, void* stream);
 
 /*
+ * ccl_gemm_splitk without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). The fp32 partial tiles go to a static
+ * device array inside the library, CCL_SCRATCH_BYTES per GPU, reserved when
+ * the library's code is loaded on that GPU and held until the process ends;
+ * the call allocates nothing. Same arithmetic, kernels and results as
+ * ccl_gemm_splitk with the same plan and splits. The array is shared by
+ * every call on one GPU and keeps the last call's partials (nothing in it
+ * has to start at zero): calls that may overlap on one GPU (different
+ * streams, several host threads) race and must be ordered by the caller.
+ * One range (splits such that a single K range results): exactly
+ * ccl_gemm_scaled, the array is not used.
+ * Errors: as ccl_gemm_splitk; CCL_ERR_INVALID_ARG also when the workspace
+ * the plan and splits need (ccl_gemm_splitk_workspace) exceeds
+ * CCL_SCRATCH_BYTES, checked before any device call.
+ */
+#define CCL_SCRATCH_BYTES (64LL << 20)
+ccl_status ccl_gemm_splitk_noalloc(ccl_plan_t plan, float alpha, const void* A_ccl,
+                                   const void* B_ccl, float beta, void* C_ccl, int splits,
+                                   void* stream);
+
+/*
  * Baseline for comparison with ccl_gemm (the layout the paper starts from,
  * Sec. II-B Eq. 2): the same GEMM kernel on plain row-major operands
  * A (M x K), B (K x N) and C (M x N), leading dimensions K, N and N, with

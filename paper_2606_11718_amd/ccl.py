@@ -17,6 +17,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libccl.so"
 
 CCL_A, CCL_B, CCL_C = 0, 1, 2
 CCL_PLACE_RR, CCL_PLACE_COARSE, CCL_PLACE_CCL = 0, 1, 2
+CCL_SCRATCH_BYTES = 64 << 20        # static split-K workspace of ccl_gemm_splitk_noalloc, per GPU
 MAX_CHIPLETS = 64
 
 STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PARTITION",
@@ -25,7 +26,7 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 # every symbol include/ccl.h declares
 EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout",
             "ccl_pack", "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_splitk_workspace",
-            "ccl_gemm_splitk", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
+            "ccl_gemm_splitk", "ccl_gemm_splitk_noalloc", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
             "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
 
 
@@ -90,6 +91,7 @@ def library() -> ctypes.CDLL:
         "ccl_gemm_scaled": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, vp],
         "ccl_gemm_splitk_workspace": [vp, ctypes.POINTER(i32), ctypes.POINTER(i64)],
         "ccl_gemm_splitk": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, i32, vp, i64, vp],
+        "ccl_gemm_splitk_noalloc": [vp, ctypes.c_float, vp, vp, ctypes.c_float, vp, i32, vp],
         "ccl_gemm_rowmajor": [vp, vp, vp, vp, i32, vp],
         "ccl_remote_bytes": [vp, i32, i32, ctypes.POINTER(_Traffic)],
         "ccl_remote_bytes_l2": [vp, i32, i32, ctypes.POINTER(_L2Config), ctypes.POINTER(_L2Traffic)],
@@ -223,6 +225,13 @@ def ccl_gemm_splitk(plan: Plan, alpha: float, A_ccl, B_ccl, beta: float, C_ccl, 
                     workspace, workspace_bytes: int, stream=None) -> None:
     _check(library().ccl_gemm_splitk(plan, alpha, _ptr(A_ccl), _ptr(B_ccl), beta, _ptr(C_ccl),
                                      splits, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def ccl_gemm_splitk_noalloc(plan: Plan, alpha: float, A_ccl, B_ccl, beta: float, C_ccl,
+                            splits: int, stream=None) -> None:
+    _check(library().ccl_gemm_splitk_noalloc(plan, ctypes.c_float(alpha), _ptr(A_ccl),
+                                             _ptr(B_ccl), ctypes.c_float(beta), _ptr(C_ccl),
+                                             splits, _stream(stream)))
 
 
 def ccl_gemm_rowmajor(plan: Plan, A, B, C, remap: int, stream=None) -> None:

@@ -268,6 +268,33 @@ ccl_status ccl_gemm_splitk(ccl_plan_t plan, float alpha, const void* A_ccl, cons
                     "split-K gemm launch");
 }
 
+ccl_status ccl_gemm_splitk_noalloc(ccl_plan_t plan, float alpha, const void* A_ccl,
+                                   const void* B_ccl, float beta, void* C_ccl, int splits,
+                                   void* stream) {
+  if (!plan || !A_ccl || !B_ccl || !C_ccl) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  if (splits < 1 || splits > ccl::kMaxSplits)
+    return fail(CCL_ERR_INVALID_ARG, "splits must be in 1..16");
+  if (ccl::effective_splits(p, splits) == 1)
+    return ccl_gemm_scaled(plan, alpha, A_ccl, B_ccl, beta, C_ccl, stream);
+  if (ccl_status st = check_split_grid(p, splits)) return st;
+  const int64_t need = ccl::splitk_workspace_bytes(p, splits);
+  if (need > ccl::kScratchBytes)
+    return fail(CCL_ERR_INVALID_ARG,
+                "split-K workspace of " + std::to_string(need) +
+                    " bytes exceeds the library's static scratch of " +
+                    std::to_string(ccl::kScratchBytes) +
+                    " bytes; use fewer splits or ccl_gemm_splitk with a caller workspace");
+  if (!aligned16(A_ccl) || !aligned16(B_ccl) || !aligned16(C_ccl))
+    return fail(CCL_ERR_MISALIGNED_POINTER, "A, B and C must be 16-byte aligned");
+  if (ccl_status s = check_device()) return s;
+  float* ws = nullptr;
+  if (ccl_status s = hip_status(ccl::scratch_workspace(&ws), "static scratch lookup")) return s;
+  return ccl_gemm_splitk(plan, alpha, A_ccl, B_ccl, beta, C_ccl, splits, ws, ccl::kScratchBytes,
+                         stream);
+}
+
 ccl_status ccl_gemm(ccl_plan_t plan, const void* A_ccl, const void* B_ccl, void* C_ccl,
                     void* stream) {
   return ccl_gemm_scaled(plan, 1.f, A_ccl, B_ccl, 0.f, C_ccl, stream);

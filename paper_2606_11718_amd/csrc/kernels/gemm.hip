@@ -34,6 +34,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 
 #include "kernels.hpp"
 
@@ -1157,6 +1158,39 @@ __global__ void __launch_bounds__(64) dispatch_probe_kernel(TileMap map, int32_t
 }
 
 }  // namespace
+
+// Split-K workspace of ccl_gemm_splitk_noalloc: the fp32 partial tiles
+// live in this array instead of caller memory. Each GPU holds its own copy
+// (allocated when the library's code object is loaded on it). Nothing in it
+// needs clearing: every K range writes its whole partial tile before the
+// reduce launch reads it. Calls that overlap on one GPU share it and race.
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::once_flag g_scratch_once[kScratchDevices];
+float* g_scratch_ptr[kScratchDevices];
+hipError_t g_scratch_err[kScratchDevices];
+}  // namespace
+
+// Host code must not pass `scratch` itself to a kernel (on the host the name
+// is only a stand-in): the device address comes from the runtime, once per
+// device, with that device current.
+hipError_t scratch_workspace(float** ws) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* ptr = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = static_cast<float*>(ptr);
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  if (g_scratch_ptr[dev] == nullptr) return hipErrorInvalidSymbol;
+  *ws = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 // Second launch of a split-K GEMM: sum the partials of every tile into C.
 static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t stream) {

@@ -33,6 +33,12 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
                        bool remap, float alpha, float beta, int splits, float* ws,
                        hipStream_t stream);
+// Split-K workspace for callers that cannot allocate device memory: a
+// static device array of kScratchBytes in the library (one per GPU, held
+// until the process ends). Returns its address on the current device,
+// looked up once per device.
+constexpr int64_t kScratchBytes = (int64_t)64 << 20;
+hipError_t scratch_workspace(float** ws);
 // Dispatch probe with the GEMM grid (4 int32 per workgroup).
 hipError_t launch_dispatch_probe(const Plan& p, int32_t* out, hipStream_t stream);
 

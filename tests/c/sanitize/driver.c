@@ -193,6 +193,15 @@ int main(void) {
          CCL_ERR_INVALID_ARG);
   EXPECT(ccl_gemm_splitk(plans[2], 1.f, P(4096), P(4096), 0.f, P(4096), 2, P(8192), ws_bytes, NULL),
          CCL_OK);
+  EXPECT(ccl_gemm_splitk_noalloc(plans[2], 1.f, P(4096), P(4096), 0.f, P(4096), 2, NULL), CCL_OK);
+  EXPECT(ccl_gemm_splitk_noalloc(plans[2], 1.f, P(4096), P(4096), 0.f, P(4096), 1, NULL), CCL_OK);
+  EXPECT(ccl_gemm_splitk_noalloc(plans[2], 1.f, P(4096), P(4096), 0.f, P(4096), 17, NULL),
+         CCL_ERR_INVALID_ARG);
+  ccl_plan_t big = NULL;
+  EXPECT(ccl_plan(4096, 4096, 8192, 8, 2, 4096, &big), CCL_OK);
+  EXPECT(ccl_gemm_splitk_noalloc(big, 1.f, P(4096), P(4096), 0.f, P(4096), 2, NULL),
+         CCL_ERR_INVALID_ARG);
+  ccl_plan_destroy(big);
   EXPECT(ccl_pack(q, CCL_A, P(4096), 2047, 0, P(4096), NULL), CCL_ERR_INVALID_ARG);
   EXPECT(ccl_pack(q, CCL_C, P(4096), 4096, 1, P(4096), NULL), CCL_ERR_INVALID_ARG);
   EXPECT(ccl_pack(q, (ccl_operand)3, P(4096), 4096, 0, P(4096), NULL), CCL_ERR_INVALID_ARG);

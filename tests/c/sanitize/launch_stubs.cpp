@@ -2,6 +2,7 @@
 // sanitizer build of the C-ABI layer instead of the HIP kernels. Each call
 // checks what a launch may rely on (pointers set, the plan's GEMM supported,
 // split-K with a workspace) and counts itself; nothing is dereferenced.
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 
@@ -43,6 +44,11 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C, con
   require(a.ld > 0 && b.ld > 0 && a.kslice > 0 && b.kslice > 0, "gemm addressing");
   require(splits >= 1 && (splits == 1 || (ws != nullptr && remap)), "split-K arguments");
   ++g_launches;
+  return hipSuccess;
+}
+
+hipError_t scratch_workspace(float** ws) {
+  *ws = reinterpret_cast<float*>(static_cast<uintptr_t>(1) << 20);   // never dereferenced
   return hipSuccess;
 }
 

@@ -105,3 +105,28 @@ def test_splitk_host_checks_pass_for_valid_calls(splits):
         msg = lib.ccl_last_error().decode()
         assert "internal" not in msg
         assert st == 5 and "hipGetDevice" in msg, msg
+
+
+def test_noalloc_splitk_host_checks():
+    """ccl_gemm_splitk_noalloc refuses, before any device call, workspaces
+    beyond the library's static scratch, bad split counts and NULL operands;
+    a request that fits gets as far as the device query."""
+    import torch
+    lib = ccl.library()
+    big = ccl.ccl_plan(4096, 4096, 8192, 8, 2, 4096)
+    splits, ws = ccl.ccl_gemm_splitk_workspace(big, 2)
+    assert splits == 2 and ws == 4096 * 4096 * 2 * 4 > ccl.CCL_SCRATCH_BYTES
+    assert lib.ccl_gemm_splitk_noalloc(big, 1.0, 4096, 4096, 0.0, 4096, 2, None) == 1
+    assert "static scratch" in lib.ccl_last_error().decode()
+    small = ccl.ccl_plan(768, 2048, 4096, 8, 1, 4096)
+    for bad in (0, 17):
+        assert lib.ccl_gemm_splitk_noalloc(small, 1.0, 4096, 4096, 0.0, 4096, bad, None) == 1
+    assert lib.ccl_gemm_splitk_noalloc(small, 1.0, None, 4096, 0.0, 4096, 2, None) == 1
+    assert lib.ccl_gemm_splitk_noalloc(small, 1.0, 4100, 4096, 0.0, 4096, 2, None) == 4
+    for splits in (1, 2, 8):                    # dW_down fits up to 10 ranges
+        assert ccl.ccl_gemm_splitk_workspace(small, splits)[1] <= ccl.CCL_SCRATCH_BYTES
+    assert ccl.ccl_gemm_splitk_workspace(small, 16)[1] > ccl.CCL_SCRATCH_BYTES
+    assert lib.ccl_gemm_splitk_noalloc(small, 1.0, 4096, 4096, 0.0, 4096, 16, None) == 1
+    if torch.cuda.device_count() == 0:          # placeholder pointers never reach a device
+        assert lib.ccl_gemm_splitk_noalloc(small, 1.0, 4096, 4096, 0.0, 4096, 2, None) == 5
+        assert "hipGetDevice" in lib.ccl_last_error().decode()
