@@ -51,9 +51,14 @@ def kernel_hash(srcs=GEMM_SRCS) -> str:
     return h.hexdigest()[:16]
 
 
+# (M K + K N + M N) * 2 bytes of either Llama forward GEMM
+ALGO_BYTES = (8192 * 8192 + 2 * 8192 * 28672) * 2
+
+
 def measured_traffic(launch_flops_unused=None):
-    """HBM bytes per GEMM launch from the committed rocprofv3 counter runs,
-    if they were taken on the current kernel source."""
+    """Bytes per GEMM launch between L2 and memory (reads and writes) from
+    the committed rocprofv3 counter runs, if they were taken on the current
+    kernel source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     t = json.load(open(TRAFFIC_FILE))
@@ -218,6 +223,12 @@ def compare_layouts(reps: int, sustained: float = 0.0, rounds: int = 1):
         B = (torch.randn(K * N, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
         C = torch.empty(M * N, device="cuda", dtype=torch.bfloat16)
         st = torch.cuda.current_stream()
+        # One pack of A (a copy of 2*M*K*2 known bytes) before the GEMMs: a
+        # reference for the memory counters of the same run.
+        Ac = torch.empty(M * K, device="cuda", dtype=torch.bfloat16)
+        ccl.ccl_pack(plans[4], ccl.CCL_A, A, K, 0, Ac, st)
+        torch.cuda.synchronize()
+        del Ac
         variants = {
             "ccl_remap_g4": lambda: ccl.ccl_gemm(plans[4], A, B, C, st),
             "ccl_remap_g8": lambda: ccl.ccl_gemm(plans[8], A, B, C, st),
@@ -607,6 +618,12 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic,
+                     "traffic_counts": ("bytes per launch between the XCDs' L2 and memory (DRAM-class "
+                                        "read requests x 128 B + write bytes), from committed rocprofv3 "
+                                        "passes on this kernel source; the Infinity Cache is on that "
+                                        "path, so an upper bound on HBM bytes"),
+                     "algorithmic_bytes": ALGO_BYTES,
+                     "traffic_over_algorithmic": (round(traffic / ALGO_BYTES, 3) if traffic else None),
                      "kernel": "gemm_kernel<256,256,%d waves> (up and down launches)" % (
                          8 if ccl.ccl_debug_gemm_config(plan_up)[:2] == (256, 256) else 4),
                      "avg_launch_ms": round(gemm_ms, 4),
