@@ -268,6 +268,53 @@ def compare_layouts(reps: int, sustained: float = 0.0, rounds: int = 1):
     return out
 
 
+def operand_diagnostic(reps: int, seconds: float):
+    """A diagnostic, not the metric: the Llama forward GEMMs (CCL operands,
+    the plan's tile map) on all-zero operands and on random operands of the
+    benchmark's distributions, in the same buffers. Zero operands hardly
+    toggle the datapaths, so the GPU keeps its top clock below the socket
+    power limit; with random operands the limit sets the clock. Per variant:
+    the median per-launch time over `reps` launches, then `seconds` of
+    back-to-back launches with the sampled clock and power."""
+    import numpy as np
+    import torch
+    from paper_2606_11718_amd import ccl
+
+    out = {}
+    for name, (M, N, K) in (("llama_up", (8192, 28672, 8192)), ("llama_down", (8192, 8192, 28672))):
+        plan = ccl.ccl_plan(M, N, K, 8, 2, 4096)
+        g = torch.Generator(device="cuda").manual_seed(11)
+        Ar = torch.randn(M * K, device="cuda", generator=g).to(torch.bfloat16)
+        Br = (torch.randn(K * N, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+        Az, Bz = torch.zeros_like(Ar), torch.zeros_like(Br)
+        C = torch.empty(M * N, device="cuda", dtype=torch.bfloat16)
+        st = torch.cuda.current_stream()
+        res = {}
+        for data, (A, B) in (("zero", (Az, Bz)), ("random", (Ar, Br))):
+            def step(_timed, A=A, B=B):
+                ccl.ccl_gemm(plan, A, B, C, st)
+            for _ in range(5):
+                step(False)
+            torch.cuda.synchronize()
+            ev = [(torch.cuda.Event(True), torch.cuda.Event(True)) for _ in range(reps)]
+            for e0, e1 in ev:
+                e0.record(st)
+                step(True)
+                e1.record(st)
+            torch.cuda.synchronize()
+            ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
+            rec = {"ms": round(ms, 4), "tflops": round(2 * M * N * K / ms / 1e9, 1),
+                   "frac": round(2 * M * N * K / ms / 1e9 / PEAK_BF16_TFLOPS, 4)}
+            if seconds > 0:
+                clk = sustained_clock(step, seconds)
+                if clk:
+                    rec["sustained"] = clk
+            res[data] = rec
+        out[name] = res
+        del Ar, Br, Az, Bz, C
+    return out
+
+
 def remote_report():
     """Remote-byte model (the library's host model) for every workload GEMM,
     grid and page size: totals per placement, floor, excess over the floor,
@@ -473,6 +520,9 @@ def main():
                     help="--compare-layouts: seconds of back-to-back launches before timing each variant")
     ap.add_argument("--rounds", type=int, default=1,
                     help="--compare-layouts: alternate the variants this many times")
+    ap.add_argument("--operand-diagnostic", action="store_true",
+                    help="only time the Llama GEMMs on zero vs random operands (a diagnostic of the "
+                         "power limit, not the metric), print one JSON line")
     ap.add_argument("--no-fp8", action="store_true", help="skip the fp8 GEMM timing")
     ap.add_argument("--fp8-only", action="store_true",
                     help="only time the fp8 GEMMs, print one JSON line")
@@ -500,6 +550,10 @@ def main():
 
     if args.compare_layouts:
         print(json.dumps({"compare_layouts": compare_layouts(args.reps, args.sustained, args.rounds)}),
+              flush=True)
+        return
+    if args.operand_diagnostic:
+        print(json.dumps({"operand_diagnostic": operand_diagnostic(args.reps, args.clock_seconds)}),
               flush=True)
         return
     if args.fp8_only:
