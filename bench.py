@@ -504,6 +504,76 @@ def workload_gemms(reps: int):
     return out
 
 
+def gemm_timeline(reps: int):
+    """Phase timeline of the bf16 GEMM on every workload shape and the Llama
+    forward pair (ccl_debug_gemm_timeline: per-wave real-time counter at
+    start, after the prologue, after the K loop, after the stores' issue;
+    shader clock over the loop). reps launches back to back after 3 warm-up
+    launches; medians over those launches of per-launch figures."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2606_11718_amd import ccl
+
+    out = {}
+    names = ["tiny", "qwen_gate_up", "qwen_dW_down", "qwen_dH", "llama_up", "llama_down"]
+    for name in names:
+        _, g = W.gemm_by_name(name)
+        plan = ccl.ccl_plan(g.M, g.N, g.K, g.chiplets, g.grids[0], 4096)
+        tm, tn, wgs = ccl.ccl_debug_gemm_config(plan)
+        lay = [ccl.ccl_plan_layout(plan, op) for op in (ccl.CCL_A, ccl.CCL_B, ccl.CCL_C)]
+        gen = torch.Generator(device="cuda").manual_seed(5)
+        A = torch.randn(lay[0].total_bytes // 2, device="cuda", generator=gen).to(torch.bfloat16)
+        B = (torch.randn(lay[1].total_bytes // 2, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        C = torch.empty(lay[2].total_bytes // 2, device="cuda", dtype=torch.bfloat16)
+        words = wgs * 8 * 8
+        tl = torch.zeros(reps * words, dtype=torch.int64, device="cuda")
+        st = torch.cuda.current_stream()
+        for _ in range(3):
+            ccl.ccl_gemm(plan, A, B, C, st)
+        for r in range(reps):
+            ccl.ccl_debug_gemm_timeline(plan, A, B, C, tl[r * words:], words * 8, st)
+        torch.cuda.synchronize()
+        rec = tl.cpu().numpy().reshape(reps, wgs, 8, 8)
+        live = rec[:, :, 0, 0] > 0
+        steps = g.K // 32
+        flop_per_step = 2 * tm * tn * 32
+        per = []
+        for r in range(reps):
+            x = rec[r][live[r]]                       # (live wgs, 8 waves, 8 words)
+            t0 = x[:, :, 0].min(1)
+            t1, t2, t3 = x[:, :, 1].max(1), x[:, :, 2].max(1), x[:, :, 3].max(1)
+            ghz = (x[:, 0, 5] - x[:, 0, 4]) / ((x[:, 0, 2] - x[:, 0, 0]) * 10.0)
+            loop_us = (t2 - t1) / 100.0
+            # gap between consecutive tiles on one CU: the next workgroup's
+            # start after the previous one's last store was issued
+            cu = x[:, 0, 6] * 65536 + (x[:, 0, 7] & 0xFF00)
+            gaps = []
+            for c in np.unique(cu):
+                sel = np.where(cu == c)[0]
+                if len(sel) > 1:
+                    o = sel[np.argsort(t0[sel])]
+                    gaps.extend((t0[o[1:]] - t3[o[:-1]]).tolist())
+            per.append({
+                "tile_gap_us": float(np.median(gaps)) / 100.0 if gaps else 0.0,
+                "span_us": (t3.max() - t0.min()) / 100.0,
+                # until the first min(workgroups, 256) workgroups (one per CU) started
+                "dispatch_us": (np.sort(t0)[min(len(t0), 256) - 1] - t0.min()) / 100.0,
+                "prologue_us": float(np.median(t1 - t0)) / 100.0,
+                "loop_us": float(np.median(loop_us)),
+                "epilogue_us": float(np.median(t3 - t2)) / 100.0,
+                "loop_clock_ghz": float(np.median(ghz)),
+                "loop_mfma_frac": float(np.median(flop_per_step / 4096.0 * steps
+                                                  / (loop_us * 1e3 * ghz))),
+            })
+        med = {k: round(float(np.median([p_[k] for p_ in per])), 3) for k in per[0]}
+        med.update({"MNK": f"{g.M}x{g.N}x{g.K}", "tile": f"{tm}x{tn}", "workgroups": wgs,
+                    "k_steps": steps, "launches": reps})
+        out[name] = med
+        del A, B, C, tl
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -528,6 +598,11 @@ def main():
                     help="only time the fp8 GEMMs, print one JSON line")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip timing the GEMM of every workload shape")
+    ap.add_argument("--workloads-only", action="store_true",
+                    help="only time the GEMM of every workload shape, print one JSON line")
+    ap.add_argument("--gemm-timeline", action="store_true",
+                    help="only record the per-workgroup phase timeline of the bf16 GEMM on the "
+                         "workload shapes, print one JSON line")
     ap.add_argument("--no-pack-hbm", action="store_true",
                     help="skip timing the pack kernels alone on rotating buffers")
     ap.add_argument("--clock-seconds", type=float, default=4.0,
@@ -558,6 +633,12 @@ def main():
         return
     if args.fp8_only:
         print(json.dumps({"fp8_gemm": fp8_gemms(args.reps)}), flush=True)
+        return
+    if args.workloads_only:
+        print(json.dumps({"workload_gemms": workload_gemms(args.reps)}), flush=True)
+        return
+    if args.gemm_timeline:
+        print(json.dumps({"gemm_timeline": gemm_timeline(args.reps)}), flush=True)
         return
 
     dev = torch.device("cuda:0")

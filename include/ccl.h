@@ -359,6 +359,26 @@ ccl_status ccl_debug_gemm_config(ccl_plan_t plan, int* tile_rows, int* tile_cols
                                  int64_t* workgroups);
 
 /*
+ * Profiling hook: ccl_gemm (same kernel, same C) on a bf16 plan, with each
+ * wave of every workgroup that has a tile recording its phase timeline.
+ * `timeline` is a device buffer of at least workgroups * waves * 64 bytes
+ * (ccl_debug_gemm_config gives the workgroups; waves per workgroup is 8,
+ * or 4 under CCL_GEMM_WAVES=4), 16-byte aligned, owned by the caller.
+ * Wave v of workgroup w writes 8 uint64 at index (w * waves + v) * 8:
+ *   0-3  the 100 MHz real-time counter at its start, after the prologue
+ *        (first stages in LDS), after the K loop and after its C stores
+ *        were issued (they complete after the wave ends, as in ccl_gemm);
+ *   4-5  the shader clock counter at its start and after the K loop;
+ *   6    the XCD id it ran on; 7 the raw HW_ID register (CU, SH, SE).
+ * Entries of workgroups without a tile are not written. Errors as
+ * ccl_gemm; CCL_ERR_UNSUPPORTED for fp8 plans; CCL_ERR_INVALID_ARG for a
+ * NULL or short timeline.
+ */
+ccl_status ccl_debug_gemm_timeline(ccl_plan_t plan, const void* A_ccl, const void* B_ccl,
+                                   void* C_ccl, uint64_t* timeline, int64_t timeline_bytes,
+                                   void* stream);
+
+/*
  * Test hook: launch a kernel with ccl_gemm's grid in which every workgroup
  * records, at out[4*wg .. 4*wg+3], the hardware XCD id it ran on, its tile
  * (tile_m, tile_n; -1 if none) and the chiplet owning that tile. `out` is a

@@ -27,7 +27,8 @@ STATUS_NAMES = {0: "CCL_OK", 1: "CCL_ERR_INVALID_ARG", 2: "CCL_ERR_UNALIGNED_PAR
 EXPORTED = ("ccl_plan", "ccl_plan_typed", "ccl_plan_destroy", "ccl_plan_grid", "ccl_plan_layout",
             "ccl_pack", "ccl_unpack", "ccl_gemm", "ccl_gemm_scaled", "ccl_gemm_splitk_workspace",
             "ccl_gemm_splitk", "ccl_gemm_splitk_noalloc", "ccl_gemm_rowmajor", "ccl_remote_bytes", "ccl_remote_bytes_l2", "ccl_status_string", "ccl_last_error",
-            "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch")
+            "ccl_debug_tile_of_wg", "ccl_debug_gemm_config", "ccl_debug_dispatch",
+            "ccl_debug_gemm_timeline")
 
 
 class CCLError(RuntimeError):
@@ -98,6 +99,7 @@ def library() -> ctypes.CDLL:
         "ccl_debug_tile_of_wg": [vp, i64, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "ccl_debug_gemm_config": [vp, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i64)],
         "ccl_debug_dispatch": [vp, vp, vp],
+        "ccl_debug_gemm_timeline": [vp, vp, vp, vp, vp, i64, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -290,3 +292,9 @@ def ccl_debug_gemm_config(plan: Plan) -> tuple[int, int, int]:
 
 def ccl_debug_dispatch(plan: Plan, out, stream=None) -> None:
     _check(library().ccl_debug_dispatch(plan, _ptr(out), _stream(stream)))
+
+
+def ccl_debug_gemm_timeline(plan: Plan, A_ccl, B_ccl, C_ccl, timeline, timeline_bytes: int,
+                            stream=None) -> None:
+    _check(library().ccl_debug_gemm_timeline(plan, _ptr(A_ccl), _ptr(B_ccl), _ptr(C_ccl),
+                                             _ptr(timeline), timeline_bytes, _stream(stream)))

@@ -407,6 +407,33 @@ ccl_status ccl_debug_gemm_config(ccl_plan_t plan, int* tile_rows, int* tile_cols
   return ok();
 }
 
+ccl_status ccl_debug_gemm_timeline(ccl_plan_t plan, const void* A_ccl, const void* B_ccl,
+                                   void* C_ccl, uint64_t* timeline, int64_t timeline_bytes,
+                                   void* stream) {
+  if (!plan || !A_ccl || !B_ccl || !C_ccl || !timeline)
+    return fail(CCL_ERR_INVALID_ARG, "NULL argument");
+  const ccl::Plan& p = plan->plan;
+  if (!p.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, p.gemm.why_unsupported);
+  if (p.ab_type != ccl::DT_BF16)
+    return fail(CCL_ERR_UNSUPPORTED, "the timeline is recorded by the bf16 GEMM kernel only");
+  const int64_t need = p.gemm.workgroups * p.gemm.waves * ccl::kTimelineWords * 8;
+  if (timeline_bytes < need)
+    return fail(CCL_ERR_INVALID_ARG, "timeline smaller than workgroups * waves * 64 bytes (" +
+                                         std::to_string(need) + ")");
+  if (!aligned16(A_ccl) || !aligned16(B_ccl) || !aligned16(C_ccl) || !aligned16(timeline))
+    return fail(CCL_ERR_MISALIGNED_POINTER, "A, B, C and the timeline must be 16-byte aligned");
+  ccl::OperandAddr a, b, c;
+  ccl_addressing(p, &a, &b, &c);
+  if (!offsets_fit(p, a, b)) return fail(CCL_ERR_UNSUPPORTED, "CCL blocks too wide for 32-bit in-tile offsets");
+  if (!addressing_in_bounds(p, a, b, c, p.lay[ccl::OP_A].total_bytes, p.lay[ccl::OP_B].total_bytes,
+                            p.lay[ccl::OP_C].total_bytes))
+    return fail(CCL_ERR_UNSUPPORTED, "internal error: GEMM addressing exceeds the CCL buffers");
+  if (ccl_status s = check_device()) return s;
+  return hip_status(ccl::launch_gemm(p, A_ccl, B_ccl, C_ccl, a, b, c, true, 1.f, 0.f, 1, nullptr,
+                                     static_cast<hipStream_t>(stream), timeline),
+                    "gemm timeline launch");
+}
+
 ccl_status ccl_debug_dispatch(ccl_plan_t plan, int32_t* out, void* stream) {
   if (!plan || !out) return fail(CCL_ERR_INVALID_ARG, "NULL argument");
   if (!plan->plan.gemm.supported) return fail(CCL_ERR_UNSUPPORTED, plan->plan.gemm.why_unsupported);

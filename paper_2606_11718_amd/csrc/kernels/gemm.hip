@@ -75,6 +75,7 @@ struct GemmParams {
   int32_t round_fast;   // bf16: K blocks and split starts are 4-step aligned (rounds path)
   int32_t splits_total; // split-K ranges per tile (reduce kernel)
   float* ws;            // split-K: fp32 partial tiles (null: write C directly)
+  uint64_t* timeline;   // bf16 kernel: kTimelineWords per wave (null: not recorded)
 };
 
 // LDS chunk swizzles (16-byte chunk index XOR a function of the row).
@@ -326,6 +327,63 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc (&acc)
   }
 }
 
+// Epilogue of the bf16 kernel for a plain bf16 C (alpha 1, beta 0, no
+// split-K), staged through LDS so that C leaves the CU in whole 128-byte
+// lines. The direct form (store_tile) writes 8 bytes per lane, i.e. 32-byte
+// pieces of 16 rows per instruction, and a CU then issues its C tile at
+// about 17 GB/s. Here each wave first writes its bf16 values into the
+// (then idle) stage buffers: rows 0 .. BM/2 - 1 of the tile into `lo`,
+// rows BM/2 .. BM - 1 into `hi`, row pitch BN * 2 bytes, with the 16-byte
+// chunk index XORed with (row mod 16) so that the 16 rows of one write fall
+// in distinct banks. Then every wave copies BM / NW whole rows to C, 16
+// bytes per lane.
+template <int BM, int BN, int NW, int TM, int TN, int WM, int WN>
+__device__ __forceinline__ void store_tile_staged(const GemmParams& p, const f32x4 (&acc)[TM][TN],
+                                                  char* lo, char* hi, int32_t pr, int32_t pc,
+                                                  int32_t ti, int32_t tj, int wm, int wn, int wave,
+                                                  int lane) {
+  constexpr int ROWB = BN * 2;              // bytes per C row in LDS and in C
+  constexpr int CPR = BN / 8;               // 16-byte chunks per row
+  constexpr int HALF = BM / 2;              // rows per half
+  constexpr int RPI = 64 / CPR;             // rows per wave-wide 16-byte access
+  constexpr int RPW = BM / NW;              // rows copied out per wave
+  static_assert(WM == HALF, "a wave's rows lie in one half");
+  static_assert(RPW % RPI == 0, "whole accesses per wave");
+  // No wave reads the stage buffers any more and no load into them is in
+  // flight (the direct-to-LDS loads of the last steps included).
+  __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  char* half = wm ? hi : lo;
+#pragma unroll
+  for (int mt = 0; mt < TM; ++mt) {
+    const int r = mt * 16 + (lane & 15);
+#pragma unroll
+    for (int nt = 0; nt < TN; ++nt) {
+      const int col = wn * WN + nt * 16 + 4 * (lane >> 4);
+      uint2 v;
+      v.x = bf16_rne(acc[mt][nt][0]) | (bf16_rne(acc[mt][nt][1]) << 16);
+      v.y = bf16_rne(acc[mt][nt][2]) | (bf16_rne(acc[mt][nt][3]) << 16);
+      *reinterpret_cast<uint2*>(half + r * ROWB + (((col >> 3) ^ (r & 15)) << 4) + ((col >> 2) & 1) * 8) = v;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  uint16_t* C = static_cast<uint16_t*>(p.C) + pr * p.c.part + pc * p.c.slice +
+                (int64_t)(ti * BM) * p.c.ld + tj * BN;
+  const int c = lane % CPR;
+#pragma unroll
+  for (int i = 0; i < RPW / RPI; ++i) {
+    const int row = wave * RPW + i * RPI + lane / CPR;
+    const int r = row % HALF;
+    const uint4 v = *reinterpret_cast<const uint4*>((row < HALF ? lo : hi) + r * ROWB + ((c ^ (r & 15)) << 4));
+    *reinterpret_cast<uint4*>(C + (int64_t)row * p.c.ld + c * 8) = v;
+  }
+}
+
 // Split-K reduction. Each tile is cut into kChunks chunks of 256 float4
 // (fragment order); workgroup w handles chunk (w >> 3) % kChunks of the tile
 // that workgroup ((w >> 3) / kChunks) * 8 + (w & 7) of the unsplit GEMM
@@ -367,6 +425,23 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmParams p) {
   store4(p, c_tile + (int64_t)m * p.c.ld + n, o);
 }
 
+// Writes one wave's phase timeline once its C stores have been issued (not
+// waited for, as in the ordinary launch): words 0-3 real-time counter
+// (start, after prologue, after K loop, after the stores' issue), 4-5
+// shader clock (start, after K loop), 6 the XCD id, 7 the raw HW_ID
+// register (its CU, SH and SE fields name the CU). Lane 0 writes.
+__device__ __forceinline__ void record_timeline(uint64_t* o, const uint64_t (&rt)[3],
+                                                const uint64_t (&clk)[2], int lane) {
+  const uint64_t t_end = __builtin_amdgcn_s_memrealtime();
+  uint32_t xcc, hw;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+  if (lane == 0) {
+    o[0] = rt[0]; o[1] = rt[1]; o[2] = rt[2]; o[3] = t_end;
+    o[4] = clk[0]; o[5] = clk[1]; o[6] = xcc; o[7] = hw;
+  }
+}
+
 template <int BM, int BN, int WGN>
 __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) {
   // The host pass only needs the launch stub; the body uses device-only
@@ -377,6 +452,16 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
   __shared__ __attribute__((aligned(1024))) char smA[NS][T::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char smB[NS][T::B_BYTES];
 
+  // Phase timeline (debug launches only; the branch is uniform): the
+  // 100 MHz real-time counter at the start, after the prologue, after the
+  // K loop and after the epilogue's stores, and the shader clock counter at
+  // the start and after the K loop.
+  const bool tl_on = p.timeline != nullptr;
+  uint64_t tl_rt[3] = {0, 0, 0}, tl_clk[2] = {0, 0};
+  if (tl_on) {
+    tl_rt[0] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[0] = __builtin_amdgcn_s_memtime();
+  }
   int32_t pr, pc, ti, tj, split;
   if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
   // K range of this workgroup: steps [k0, k0 + ksteps) (all of K without split-K)
@@ -595,6 +680,7 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j) load_stage(smA[j], smB[j], j < ksteps);
   stage_barrier();
+  if (tl_on) tl_rt[1] = __builtin_amdgcn_s_memrealtime();
 #pragma unroll
   for (int mt = 0; mt < kHalfM; ++mt) read_a(smA[0], mt);
 #pragma unroll
@@ -642,7 +728,19 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
       if (s + j < ksteps) single_step(j, s + j);
   }
 
-  store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  if (tl_on) {
+    tl_rt[2] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[1] = __builtin_amdgcn_s_memtime();
+  }
+  static_assert((BM / 2) * BN * 2 <= NS * T::A_BYTES && (BM / 2) * BN * 2 <= NS * T::B_BYTES,
+                "each half of the bf16 C tile fits in one operand's stage buffers");
+  if (p.epi == 0 && !p.c_f32 && !p.ws)
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
+                                                                 pc, ti, tj, wm, wn, wave, lane);
+  else
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  if (tl_on) record_timeline(p.timeline + ((int64_t)blockIdx.x * T::NW + wave) * kTimelineWords,
+                             tl_rt, tl_clk, lane);
 #endif
 }
 
@@ -1223,9 +1321,10 @@ static hipError_t launch_splitk_reduce(const Plan& p, GemmParams gp, hipStream_t
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
                        bool remap, float alpha, float beta, int splits, float* ws,
-                       hipStream_t stream) {
+                       hipStream_t stream, uint64_t* timeline) {
   const GemmConfig& g = p.gemm;
   GemmParams gp;
+  gp.timeline = timeline;
   gp.A = static_cast<const uint16_t*>(A);
   gp.B = static_cast<const uint16_t*>(B);
   gp.C = C;
@@ -1237,6 +1336,7 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
   splits = effective_splits(p, splits);      // every K range non-empty
   gp.map = tile_map(p, splits);
   const bool fp8 = p.ab_type == DT_FP8_E4M3;
+  if (timeline && (fp8 || splits > 1)) return hipErrorInvalidValue;   // bf16 kernel only
   gp.ksteps = (int32_t)(p.K / (fp8 ? kBK8 : kBK));
   gp.ksteps_per_split = (gp.ksteps + splits - 1) / splits;
   // Rounds path of the bf16 kernel: each operand's K blocks are a multiple

@@ -29,10 +29,13 @@ hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld,
 // C = alpha A B + beta C with the given operand addressing; remap =
 // XCD-aware tile map. C is read only when beta != 0. splits > 1 (remap
 // only): split-K into the fp32 workspace ws, then a reduce launch.
+// timeline (bf16, unsplit only): kTimelineWords uint64 per wave of every
+// workgroup that has a tile, recorded by the kernel (debug launches).
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
                        const OperandAddr& a, const OperandAddr& b, const OperandAddr& c,
                        bool remap, float alpha, float beta, int splits, float* ws,
-                       hipStream_t stream);
+                       hipStream_t stream, uint64_t* timeline = nullptr);
+constexpr int kTimelineWords = 8;
 // Split-K workspace for callers that cannot allocate device memory: a
 // static device array of kScratchBytes in the library (one per GPU, held
 // until the process ends). Returns its address on the current device,

@@ -210,6 +210,15 @@ int main(void) {
   EXPECT(ccl_unpack(q, CCL_C, P(4096), P(4096), 1535, NULL), CCL_ERR_INVALID_ARG);
   EXPECT(ccl_unpack(q, CCL_C, P(4096), P(4096), 1536, NULL), CCL_OK);
   EXPECT(ccl_debug_dispatch(q, P(4096), NULL), CCL_OK);
+  int tl_rows = 0, tl_cols = 0;
+  int64_t tl_wgs = 0;
+  EXPECT(ccl_debug_gemm_config(q, &tl_rows, &tl_cols, &tl_wgs), CCL_OK);
+  EXPECT(ccl_debug_gemm_timeline(q, P(4096), P(4096), P(4096), (uint64_t*)P(4096),
+                                 tl_wgs * 8 * 64 - 8, NULL),
+         CCL_ERR_INVALID_ARG);
+  EXPECT(ccl_debug_gemm_timeline(q, P(4096), P(4096), P(4096), (uint64_t*)P(4096),
+                                 tl_wgs * 8 * 64, NULL),
+         CCL_OK);
   ccl_plan_t longb = NULL;
   EXPECT(ccl_plan(128, 128 * 140000, 128, 1, 1, 4096, &longb), CCL_OK);
   EXPECT(ccl_gemm(longb, P(4096), P(4096), P(4096), NULL), CCL_ERR_UNSUPPORTED);

@@ -39,8 +39,9 @@ hipError_t launch_pack_trans(const Plan& p, int op, const void* src, int64_t ld,
 
 hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C, const OperandAddr& a,
                        const OperandAddr& b, const OperandAddr&, bool remap, float, float,
-                       int splits, float* ws, hipStream_t) {
+                       int splits, float* ws, hipStream_t, uint64_t* timeline) {
   require(A && B && C && p.gemm.supported, "gemm arguments");
+  require(!timeline || (splits == 1 && p.ab_type == DT_BF16), "timeline arguments");
   require(a.ld > 0 && b.ld > 0 && a.kslice > 0 && b.kslice > 0, "gemm addressing");
   require(splits >= 1 && (splits == 1 || (ws != nullptr && remap)), "split-K arguments");
   ++g_launches;

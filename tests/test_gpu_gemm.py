@@ -92,6 +92,18 @@ def test_gemm_every_kernel_variant(tile, waves, M, N, K, G, Gr):
     _check_full(A, 0, B, 0, M, N, K, G, Gr, 4096, tile, waves)
 
 
+@pytest.mark.parametrize("tile", ["256x128", "128x256", "128x128"])
+@pytest.mark.parametrize("steps", [1, 2, 3, 5, 7, 12, 13, 19, 28, 45])
+def test_gemm_stage_ring_step_counts(tile, steps):
+    """K step counts that stop inside the first lone step, the first
+    rounds, the loop and the tail of the rounds path of the smaller tiles
+    (one chiplet, so one K block per operand)."""
+    M, N, K = 256, 256, 32 * steps
+    A = W.draw_array(951 + steps, M, K, "normal", 1.0)
+    B = W.draw_array(952 + steps, K, N, "normal", 0.05)
+    _check_full(A, 0, B, 0, M, N, K, 1, 1, 4096, tile, 8)
+
+
 @pytest.mark.parametrize("M,N,K,G,Gr,P,ta,tb", [
     (256, 512, 256, 4, 2, 65536, 0, 0),          # padded strips
     (256, 512, 256, 4, 2, 2 * 1024 * 1024, 0, 1),

@@ -74,7 +74,7 @@ def _plans():
 def test_no_mismatch_and_every_valid_device_call_reached_its_launcher(run):
     assert run["failures"] == [["0"]]
     assert "MISMATCH" not in run
-    assert run["launches"] == [["10"]]
+    assert run["launches"] == [["11"]]
 
 
 def test_plans_layouts_and_traffic_equal_the_library(run):

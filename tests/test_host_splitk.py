@@ -130,3 +130,25 @@ def test_noalloc_splitk_host_checks():
     if torch.cuda.device_count() == 0:          # placeholder pointers never reach a device
         assert lib.ccl_gemm_splitk_noalloc(small, 1.0, 4096, 4096, 0.0, 4096, 2, None) == 5
         assert "hipGetDevice" in lib.ccl_last_error().decode()
+
+
+def test_gemm_timeline_host_checks():
+    """ccl_debug_gemm_timeline refuses, before any device call, NULL
+    arguments, a timeline shorter than workgroups * waves * 64 bytes,
+    misaligned pointers and fp8 plans."""
+    import torch
+    lib = ccl.library()
+    p = ccl.ccl_plan(768, 2048, 4096, 8, 1, 4096)
+    _, _, wgs = ccl.ccl_debug_gemm_config(p)
+    need = wgs * 8 * 64
+    call = lambda tl, nb, a=4096: lib.ccl_debug_gemm_timeline(p, a, 4096, 4096, tl, nb, None)
+    assert call(None, need) == 1
+    assert call(4096, need - 1) == 1
+    assert "timeline smaller" in lib.ccl_last_error().decode()
+    assert call(4104, need) == 4
+    assert call(4096, need, a=4100) == 4
+    f8 = ccl.ccl_plan_typed(768, 2048, 4096, 8, 1, 4096, FP8, BF16)
+    assert lib.ccl_debug_gemm_timeline(f8, 4096, 4096, 4096, 4096, need, None) == 3
+    if torch.cuda.device_count() == 0:          # placeholder pointers never reach a device
+        assert call(4096, need) == 5
+        assert "hipGetDevice" in lib.ccl_last_error().decode()
