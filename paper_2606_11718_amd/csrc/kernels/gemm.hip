@@ -327,8 +327,8 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc (&acc)
   }
 }
 
-// Epilogue of the bf16 kernel for a plain bf16 C (alpha 1, beta 0, no
-// split-K), staged through LDS so that C leaves the CU in whole 128-byte
+// Epilogue of the kernels with 16x16 MFMA tiles (bf16, fp8 16x16x128) for a
+// plain bf16 C (alpha 1, beta 0, no split-K), staged through LDS so that C leaves the CU in whole 128-byte
 // lines. The direct form (store_tile) writes 8 bytes per lane, i.e. 32-byte
 // pieces of 16 rows per instruction, and a CU then issues its C tile at
 // about 17 GB/s. Here each wave first writes its bf16 values into the
@@ -1233,7 +1233,13 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8x_kernel(GemmParam
     step(0, false);
   }
 
-  store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  static_assert((BM / 2) * BN * 2 <= 2 * T::A_BYTES && (BM / 2) * BN * 2 <= 2 * T::B_BYTES,
+                "each half of the bf16 C tile fits in one operand's stage buffers");
+  if (p.epi == 0 && !p.c_f32 && !p.ws)
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
+                                                                 pc, ti, tj, wm, wn, wave, lane);
+  else
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
 #endif
 }
 
