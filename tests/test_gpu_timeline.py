@@ -43,9 +43,15 @@ def test_timeline_matches_gemm_and_is_well_formed(M, N, K, G, Gr):
     assert np.all(r[:, :, 5] > r[:, :, 4])                       # clock advanced over the loop
     assert np.all(r[:, :, 6] == r[:, :1, 6])                     # one XCD and one CU per workgroup
     assert np.all(r[:, :, 7] & 0xFF00 == r[:, :1, 7] & 0xFF00)
+    # Round-robin dispatch: workgroup w on XCD (w + rot) mod 8, one rotation
+    # for the launch (0 in nearly every launch; see test_gpu_gemm's probe).
+    xcc = r[:, 0, 6] & 0xF
+    rot = (xcc - np.array(live)) % 8
+    print("dispatch rotation", sorted(set(rot.tolist())), flush=True)
+    assert len(set(rot.tolist())) == 1
     for w, row in zip(live, r):
         xcd, ti, tj = ccl.ccl_debug_tile_of_wg(plan, w)
-        assert row[0, 6] == xcd == w % 8
+        assert xcd == w % 8 and (row[0, 6] & 0xF) == (xcd + rot[0]) % 8
         owner = OP.owner(ti * tm_ // 128, tj * tn_ // 128, M, N, Gr, G // Gr)
         assert xcd in OP.xcds_of_chiplet(owner, G)
     # the clock implied by the loop (shader cycles over 100 MHz ticks) is a
