@@ -179,11 +179,11 @@ def test_gemm_llama_backward_grid_sweep_full_compare(gemm):
                                         (1024, 1024, 1024, 1, 1), (1024, 2048, 512, 2, 1)])
 def test_dispatch_probe_tiles_run_on_owner_xcd(M, N, K, G, Gr):
     """Hardware check of the remap: workgroups are dispatched round-robin
-    over the 8 XCDs (workgroup w on XCD (w + rot) mod 8 with one rotation
-    per launch; rot was 0 in every launch of these tests but one, in a full
-    run after the graph-replay tests), so the workgroups the map gives one
-    chiplet's tiles share one XCD; with rot = 0 that XCD is the owner's.
-    Every tile is computed exactly once."""
+    over the 8 XCDs (workgroup w on XCD (w + rot) mod 8, where rot depends
+    on the hardware queue behind the stream: 0 for the null stream of a
+    fresh process, other values once more streams exist), so the
+    workgroups the map gives one chiplet's tiles share one XCD; with
+    rot = 0 that XCD is the owner's. Every tile is computed exactly once."""
     torch = __import__("torch")
     plan = ccl.ccl_plan(M, N, K, G, Gr, 4096)
     tm_, tn_, wgs = ccl.ccl_debug_gemm_config(plan)

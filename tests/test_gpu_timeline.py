@@ -44,7 +44,7 @@ def test_timeline_matches_gemm_and_is_well_formed(M, N, K, G, Gr):
     assert np.all(r[:, :, 6] == r[:, :1, 6])                     # one XCD and one CU per workgroup
     assert np.all(r[:, :, 7] & 0xFF00 == r[:, :1, 7] & 0xFF00)
     # Round-robin dispatch: workgroup w on XCD (w + rot) mod 8, one rotation
-    # for the launch (0 in nearly every launch; see test_gpu_gemm's probe).
+    # for the launch, set by the hardware queue behind the stream.
     xcc = r[:, 0, 6] & 0xF
     rot = (xcc - np.array(live)) % 8
     print("dispatch rotation", sorted(set(rot.tolist())), flush=True)
