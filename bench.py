@@ -456,7 +456,9 @@ def pack_hbm(reps: int):
 def workload_gemms(reps: int):
     """Per-launch time of ccl_gemm on every workload GEMM shape (bf16, random
     operands already in CCL), at the grid the parity tests use: the small
-    Qwen3 shapes, the tiny case and the Llama backward GEMMs."""
+    Qwen3 shapes, the tiny case and the Llama backward GEMMs. Beside each,
+    torch.matmul of row-major operands of the same shape (the vendor BLAS,
+    free to use every CU) timed the same way."""
     import numpy as np
     import torch
     import workloads as W
@@ -491,6 +493,16 @@ def workload_gemms(reps: int):
             tm, tn, _ = ccl.ccl_debug_gemm_config(plan)
             rec = {"MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
                    "ms": round(ms, 4), "tflops": round(g.flops / ms / 1e9, 1)}
+            # the vendor library on the same shape, box and power limit:
+            # torch.matmul of contiguous row-major bf16 operands
+            Ar = torch.randn(g.M, g.K, device="cuda", generator=gen).to(torch.bfloat16)
+            Br = (torch.randn(g.K, g.N, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+            Cr = torch.empty(g.M, g.N, device="cuda", dtype=torch.bfloat16)
+            ms_v = timed(lambda: torch.matmul(Ar, Br, out=Cr))
+            rec["vendor_matmul"] = {"ms": round(ms_v, 4), "tflops": round(g.flops / ms_v / 1e9, 1),
+                                    "ccl_speedup": round(ms_v / ms, 3),
+                                    "blas": str(torch.backends.cuda.preferred_blas_library())}
+            del Ar, Br, Cr
             ranges, ws_bytes = ccl.ccl_gemm_splitk_workspace(plan, 0)
             if ranges > 1:             # the library's split-K choice for this shape
                 ws = torch.empty(ws_bytes, device="cuda", dtype=torch.uint8)
