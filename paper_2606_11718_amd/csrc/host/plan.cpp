@@ -145,6 +145,18 @@ void choose_gemm_config(Plan* p) {
   g.waves = eight_ok ? 8 : 4;
   if (const char* e = std::getenv("CCL_GEMM_WAVES"))
     g.waves = (std::atoi(e) == 8 && eight_ok) ? 8 : 4;
+  // LDS stage depth in K (bf16). A stage of 32 K holds 64-byte A rows, half
+  // a 128-byte line, and a CU streams such half lines from L2 at 36-47
+  // B/clk when most CUs load, against 57-64 B/clk for whole lines
+  // (direct-to-LDS loads of L2-resident data). The tiles below 256x256 need
+  // 48-64 B/clk per CU at the matrix cores' rate, so they take 64-K stages
+  // (whole-line A rows), where both K blocks allow it. 256x256 keeps 32:
+  // two 64-K stages would leave one step of load lookahead.
+  // CCL_GEMM_STAGE_K=32 selects the 32-K stages everywhere.
+  g.stage_k = (p->ab_type == DT_BF16 && g.waves == 8 && !(btm == 256 && btn == 256) &&
+               (p->K / p->Gc) % 64 == 0 && (p->K / p->Gr) % 64 == 0) ? 64 : 32;
+  if (const char* e = std::getenv("CCL_GEMM_STAGE_K"))
+    if (std::atoi(e) == 32) g.stage_k = 32;
   if (g.workgroups > 0x7fffffff) {
     g.why_unsupported = "launch too large";
     return;

@@ -745,6 +745,325 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_kernel(GemmParams p) 
 }
 
 // ---------------------------------------------------------------------------
+// bf16 with 64-K stages, for the output tiles below 256x256 (8 waves). A
+// stage holds 64 K, so each A row in LDS is 128 bytes: the
+// direct-to-LDS loads fetch whole 128-byte lines of A, which a CU streams
+// from L2 about 1.5x faster than the half lines of 32-K stages when most
+// CUs load at once. Each step runs the MFMAs of two 32-K sub-steps (kk = 0,
+// 1) around one barrier:
+//  * first half: the MFMAs of sub-step 0 (fragments fa0/fb0), behind them
+//    the reads of sub-step 1's fragments (fa1/fb1) and the direct-to-LDS
+//    loads of the stage NS-1 steps ahead;
+//  * stage barrier;
+//  * second half: the MFMAs of sub-step 1, behind them the reads of the next
+//    stage's sub-step 0 fragments into fa0/fb0.
+// A rows: chunk c (16 bytes) of row r sits at chunk c ^ swz_a64(r); the 16
+// rows x 4 chunks of one A fragment read then fall in distinct bank slots
+// (checked against the measured ds_read_b128 grouping: lanes with equal
+// parity of lane bits 2..4 are served together). B rows are as in the 32-K
+// kernel, twice as many per stage.
+// ---------------------------------------------------------------------------
+
+constexpr int kBK64 = 64;        // K extent of one stage of gemm_k64_kernel
+
+__device__ __forceinline__ int swz_a64(int row) { return (row >> 1) & 7; }
+
+template <int BM, int BN>
+struct Tile64 {
+  static constexpr int WGN = 4;
+  static constexpr int NW = 8;                         // waves per workgroup
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;     // wave tile
+  static constexpr int TM = WM / 16, TN = WN / 16;     // MFMA tiles per wave
+  static constexpr int A_BYTES = BM * kBK64 * 2;       // one stage
+  static constexpr int B_BYTES = kBK64 * BN * 2;
+  static constexpr int NA = A_BYTES / (1024 * NW);     // A loads per wave per stage (8 rows each)
+  static constexpr int CPR_B = BN / 8;                 // 16-byte chunks per B row
+  static constexpr int RPI_B = 64 / CPR_B;             // B rows per load instruction
+  static constexpr int NB = B_BYTES / (1024 * NW);     // B loads per wave per stage
+  static constexpr int NL = NA + NB;
+  // as many stages as 160 KiB holds, at most 4: 3 for 256x128 and
+  // 128x256, 4 for 128x128
+  static constexpr int NS = (160 * 1024) / (A_BYTES + B_BYTES) >= 4 ? 4 : 3;
+  static_assert(BM * BN < 256 * 256, "256x256 tiles use the 32-K stages");
+  static_assert(NA >= 1 && NB >= 1 && TN >= 1 && TM >= 1, "tile too small for the wave grid");
+  static_assert(NS * (A_BYTES + B_BYTES) <= 160 * 1024, "LDS stages exceed 160 KiB");
+  static_assert((NS - 2) * NL <= 63, "the stage wait count exceeds vmcnt's range");
+  static_assert(BN == 128 || BN == 256, "B swizzle is defined for 16- and 32-chunk rows");
+};
+
+template <int BM, int BN>
+__global__ void __launch_bounds__(512, 2) gemm_k64_kernel(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using T = Tile64<BM, BN>;
+  constexpr int NS = T::NS;
+  __shared__ __attribute__((aligned(1024))) char smA[NS][T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[NS][T::B_BYTES];
+
+  const bool tl_on = p.timeline != nullptr;
+  uint64_t tl_rt[3] = {0, 0, 0}, tl_clk[2] = {0, 0};
+  if (tl_on) {
+    tl_rt[0] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[0] = __builtin_amdgcn_s_memtime();
+  }
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  // K range of this workgroup: steps [k0, k0 + ksteps) (all of K without split-K)
+  const int32_t k0 = __builtin_amdgcn_readfirstlane(split * p.ksteps_per_split);
+  const int32_t ksteps = __builtin_amdgcn_readfirstlane(min(p.ksteps, k0 + p.ksteps_per_split) - k0);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
+
+  // ---- global -> LDS: per-lane byte offsets from the K step's tile corner ----
+  // A load i of this wave fills LDS rows 8*(wave*NA+i) .. +7 (128 B each);
+  // the lane at LDS chunk q of its row fetches global chunk q ^ swz_a64(row).
+  uint32_t a_voff[T::NA];
+#pragma unroll
+  for (int i = 0; i < T::NA; ++i) {
+    const int row = 8 * (wave * T::NA + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz_a64(row);
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
+  }
+  uint32_t b_voff[T::NB];
+#pragma unroll
+  for (int i = 0; i < T::NB; ++i) {
+    const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
+    const int chunk = (lane % T::CPR_B) ^ swz_b(row);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 8) * 2u;
+  }
+  const int32_t a_extent = (BM - 1) * p.a.ld * 2 + kBK64 * 2;
+  const int32_t b_extent = (kBK64 - 1) * p.b.ld * 2 + BN * 2;
+
+  // ---- LDS fragment read offsets (bytes), sub-step kk ----
+  // A fragment of MFMA tile mt: lane l reads row wm*WM + 16 mt + l % 16,
+  // K chunk 4 kk + l / 16; the swizzle depends on the row only through
+  // (row >> 1) & 7, the same for every mt.
+  int32_t a_rd[2];
+  {
+    const int row = wm * T::WM + (lane & 15);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      a_rd[kk] = row * 128 + (((4 * kk + (lane >> 4)) ^ swz_a64(row)) * 16);
+  }
+  int32_t b_rd[T::TN][2];
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int nt = 0; nt < T::TN; ++nt) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int krow = 8 * g + 4 * r + (s >> 2);
+        const int col = wn * T::WN + nt * 16 + 4 * (s & 3);
+        b_rd[nt][r] = krow * (BN * 2) + (((col >> 3) ^ swz_b(krow)) * 16) + ((col >> 2) & 1) * 8;
+      }
+    }
+  }
+  constexpr int kB_KK = 32 * BN * 2;            // bytes between the two sub-steps' B rows
+
+  // ---- operand corners; K-slice block advances every kslice columns/rows ----
+  const uint16_t* a_base = p.A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
+  const uint16_t* b_base = p.B + pc * p.b.part + tj * BN;
+  int64_t a_slice_off, b_slice_off;
+  int32_t a_kl, b_kl;
+  k_start(p.a, k0 * kBK64, &a_slice_off, &a_kl);
+  k_start(p.b, k0 * kBK64, &b_slice_off, &b_kl);
+  const char* a_next = reinterpret_cast<const char*>(a_base + a_slice_off + a_kl);
+  const char* b_next = reinterpret_cast<const char*>(b_base + b_slice_off + (int64_t)b_kl * p.b.ld);
+  const int32_t a_steps = p.a.kslice / kBK64, b_steps = p.b.kslice / kBK64;
+  int32_t a_left = a_steps - a_kl / kBK64, b_left = b_steps - b_kl / kBK64;
+  const int64_t a_adv = kBK64 * 2, b_adv = (int64_t)kBK64 * p.b.ld * 2;
+  const int64_t a_jump = (p.a.slice - p.a.kslice) * 2;
+  const int64_t b_jump = (p.b.slice - (int64_t)p.b.kslice * p.b.ld) * 2;
+
+  struct StageSrc {
+    i32x4 ra, rb;
+  };
+  auto next_src = [&](bool live) {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
+    const bool a_wrap = --a_left == 0;
+    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left;
+    const bool b_wrap = --b_left == 0;
+    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left;
+    return d;
+  };
+  const int32_t a_extent4 = (BM - 1) * p.a.ld * 2 + 4 * kBK64 * 2;
+  const int32_t b_extent4 = (4 * kBK64 - 1) * p.b.ld * 2 + BN * 2;
+  const uint32_t so_a[4] = {0u, (uint32_t)a_adv, (uint32_t)(2 * a_adv), (uint32_t)(3 * a_adv)};
+  const uint32_t so_b[4] = {0u, (uint32_t)b_adv, (uint32_t)(2 * b_adv), (uint32_t)(3 * b_adv)};
+  auto round_src = [&]() {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_next, a_extent4);
+    d.rb = buffer_rsrc(b_next, b_extent4);
+    const bool a_wrap = a_left == 4;
+    a_next += 4 * a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left - 4;
+    const bool b_wrap = b_left == 4;
+    b_next += 4 * b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left - 4;
+    return d;
+  };
+  auto load_one = [&](const StageSrc& d, int j, char* sA, char* sB, int i) {
+    if (i < T::NA) {
+      char* dst = sA + (wave * T::NA + i) * 1024;
+      if (j < 0) lds_dma16(d.ra, a_voff[i], dst);
+      else lds_dma16_so(d.ra, a_voff[i], so_a[j], dst);
+    } else {
+      char* dst = sB + (wave * T::NB + (i - T::NA)) * 1024;
+      if (j < 0) lds_dma16(d.rb, b_voff[i - T::NA], dst);
+      else lds_dma16_so(d.rb, b_voff[i - T::NA], so_b[j], dst);
+    }
+  };
+  auto load_stage = [&](char* sA, char* sB, bool live) {
+    const StageSrc d = next_src(live);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d, -1, sA, sB, i);
+  };
+
+  AFrags<T::TM> fa0, fa1;
+  BFrags<T::TN> fb0, fb1;
+  auto read_a = [&](const char* sA, AFrags<T::TM>& fa, int kk, int mt) {
+    fa.a[mt] = *(const lds_bf16x8*)(sA + a_rd[kk] + mt * 16 * 128);
+  };
+  auto read_b = [&](const char* sB, BFrags<T::TN>& fb, int kk, int i) {
+    const int nt = i >> 1, r = i & 1;
+    fb.b[nt][r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sB + b_rd[nt][r] + kk * kB_KK));
+  };
+
+  f32x4 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+
+  auto mfma_one = [&](const AFrags<T::TM>& fa, const BFrags<T::TN>& fb, int mt, int nt) {
+    const bf16x8 bv = __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(fb.b[nt][0], fb.b[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
+    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv, fa.a[mt], acc[mt][nt], 0, 0, 0);
+  };
+  auto stage_barrier = [&]() {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm((NS - 2) * T::NL, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // One step on stage (sA, sB); on entry fa0/fb0 hold its sub-step 0.
+  auto step = [&](const char* sA, const char* sB, char* lA, char* lB, const char* nA,
+                  const char* nB, const StageSrc& d, int j) {
+    constexpr int kMfma = T::TM * T::TN;
+    constexpr int kReads = T::TM + 2 * T::TN;
+    constexpr int kOps1 = kReads + T::NL;
+#pragma unroll
+    for (int i = 0; i < kMfma; ++i) {
+      mfma_one(fa0, fb0, i / T::TN, i % T::TN);
+      if (i < T::TM) read_a(sA, fa1, 1, i);
+      else if (i < kReads) read_b(sB, fb1, 1, i - T::TM);
+      else if (i < kOps1) load_one(d, j, lA, lB, i - kReads);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfma; i < kOps1; ++i) {
+      if (i < T::TM) read_a(sA, fa1, 1, i);
+      else if (i < kReads) read_b(sB, fb1, 1, i - T::TM);
+      else load_one(d, j, lA, lB, i - kReads);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    stage_barrier();
+#pragma unroll
+    for (int i = 0; i < kMfma; ++i) {
+      mfma_one(fa1, fb1, i / T::TN, i % T::TN);
+      if (i < T::TM) read_a(nA, fa0, 0, i);
+      else if (i < kReads) read_b(nB, fb0, 0, i - T::TM);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfma; i < kReads; ++i) {
+      if (i < T::TM) read_a(nA, fa0, 0, i);
+      else read_b(nB, fb0, 0, i - T::TM);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Prologue: the first NS-1 stages in flight, then stage 0's sub-step 0.
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) load_stage(smA[j], smB[j], j < ksteps);
+  stage_barrier();
+  if (tl_on) tl_rt[1] = __builtin_amdgcn_s_memrealtime();
+#pragma unroll
+  for (int mt = 0; mt < T::TM; ++mt) read_a(smA[0], fa0, 0, mt);
+#pragma unroll
+  for (int i = 0; i < 2 * T::TN; ++i) read_b(smB[0], fb0, 0, i);
+  // Step s works on stage s % NS, loads stage (s + NS - 1) % NS and reads
+  // stage (s + 1) % NS; ph is s modulo a multiple of NS.
+  auto phase_step = [&](int ph, const StageSrc& d, int j) {
+    step(smA[ph % NS], smB[ph % NS], smA[(ph + NS - 1) % NS], smB[(ph + NS - 1) % NS],
+         smA[(ph + 1) % NS], smB[(ph + 1) % NS], d, j);
+  };
+  auto single_step = [&](int ph, int32_t s) {
+    const StageSrc d = next_src(s + NS - 1 < ksteps);
+    phase_step(ph, d, -1);
+  };
+  int32_t s = 0;
+  if (p.round_fast) {
+    // Rounds of 4 steps whose loads (steps s+NS-1 .. s+NS+2) form a
+    // 4-aligned group, all live, sharing one pair of descriptors. The first
+    // kFirst steps run alone so that the first round's loads start
+    // 4-aligned; a loop iteration runs kLoop steps (a multiple of NS and of
+    // 4, so every phase is known at compile time); the remaining steps
+    // (fewer than kLoop + NS - 1) run alone.
+    constexpr int kFirst = (4 - (NS - 1) % 4) % 4;
+    constexpr int kLoop = NS % 4 == 0 ? NS : 4 * NS;
+#pragma unroll
+    for (int t = 0; t < kFirst; ++t)
+      if (t < ksteps) single_step(t, t);
+    for (s = kFirst; s + kLoop + NS - 1 <= ksteps; s += kLoop) {
+#pragma unroll
+      for (int r = 0; r < kLoop / 4; ++r) {
+        const StageSrc d = round_src();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) phase_step(kFirst + 4 * r + j, d, j);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kLoop + NS - 2; ++t)
+      if (s + t < ksteps) single_step(kFirst + t, s + t);
+  } else {
+    const int32_t full = ksteps - ksteps % NS;
+    for (; s < full; s += NS) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) single_step(j, s + j);
+    }
+#pragma unroll
+    for (int j = 0; j < NS - 1; ++j)
+      if (s + j < ksteps) single_step(j, s + j);
+  }
+
+  if (tl_on) {
+    tl_rt[2] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[1] = __builtin_amdgcn_s_memtime();
+  }
+  static_assert((BM / 2) * BN * 2 <= NS * T::A_BYTES && (BM / 2) * BN * 2 <= NS * T::B_BYTES,
+                "each half of the bf16 C tile fits in one operand's stage buffers");
+  if (p.epi == 0 && !p.c_f32 && !p.ws)
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
+                                                                 pc, ti, tj, wm, wn, wave, lane);
+  else
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  if (tl_on) record_timeline(p.timeline + ((int64_t)blockIdx.x * T::NW + wave) * kTimelineWords,
+                             tl_rt, tl_clk, lane);
+#endif
+}
+
+// ---------------------------------------------------------------------------
 // fp8 (E4M3) operands: C = A B with v_mfma_f32_32x32x64_f8f6f4 (unscaled).
 // A K step is 64 fp8 elements, so one stage holds the same bytes as a bf16
 // step (A rows of 64 bytes, B rows of BN bytes x 64 rows) and the A side
@@ -1394,6 +1713,36 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
       return hipErrorInvalidValue;
 #undef CCL_LAUNCH8
     return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
+  }
+  // 64-K stages (plan's choice for the bf16 tiles below 256x256): both K
+  // blocks a multiple of 64, the 4-step rounds' extents (255 rows of A or
+  // B) within 32-bit offsets, and with split-K only where the K ranges are
+  // the 32-K ranges (each range an even number of 32-K steps), so the
+  // workspace and the reduce are unchanged.
+  {
+    const int64_t lim = ((int64_t)1 << 31) - 4096;
+    const int32_t ks64 = (int32_t)(p.K / kBK64);
+    const int32_t per64 = (ks64 + splits - 1) / splits;
+    const bool k64 = g.stage_k == 64 && !fp8 && waves == 8 &&
+                     !(g.tile_m == 256 && g.tile_n == 256) && a.kslice % kBK64 == 0 &&
+                     b.kslice % kBK64 == 0 && 255 * (int64_t)a.ld * 2 + 512 < lim &&
+                     255 * (int64_t)b.ld * 2 + 512 < lim && 2 * per64 == gp.ksteps_per_split;
+    if (k64) {
+      const auto aligned64 = [&](const OperandAddr& o) {
+        return (int64_t)o.kslice == p.K || (o.kslice / kBK64) % 4 == 0;
+      };
+      gp.ksteps = ks64;
+      gp.ksteps_per_split = per64;
+      gp.round_fast = aligned64(a) && aligned64(b) && (splits == 1 || per64 % 4 == 0) ? 1 : 0;
+#define CCL_LAUNCH64(BM_, BN_)                                                                \
+  hipLaunchKernelGGL((gemm_k64_kernel<BM_, BN_>), grid, dim3(Tile64<BM_, BN_>::THREADS), 0, stream, gp)
+      if (g.tile_m == 256 && g.tile_n == 128) CCL_LAUNCH64(256, 128);
+      else if (g.tile_m == 128 && g.tile_n == 256) CCL_LAUNCH64(128, 256);
+      else if (g.tile_m == 128 && g.tile_n == 128) CCL_LAUNCH64(128, 128);
+      else return hipErrorInvalidValue;
+#undef CCL_LAUNCH64
+      return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
+    }
   }
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \

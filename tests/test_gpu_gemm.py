@@ -104,6 +104,52 @@ def test_gemm_stage_ring_step_counts(tile, steps):
     _check_full(A, 0, B, 0, M, N, K, 1, 1, 4096, tile, 8)
 
 
+def _run_stage_k(stage_k, A, B, M, N, K, G, Gr, tile):
+    if stage_k == 32:
+        os.environ["CCL_GEMM_STAGE_K"] = "32"
+    try:
+        Cbits, _ = run_gemm(A, 0, B, 0, M, N, K, G, Gr, 4096, tile, waves=8)
+    finally:
+        os.environ.pop("CCL_GEMM_STAGE_K", None)
+    return Cbits
+
+
+@pytest.mark.parametrize("tile", ["256x128", "128x256", "128x128"])
+@pytest.mark.parametrize("M,N,K,G,Gr", [(4096, 1536, 2048, 8, 2),     # Qwen3 gate/up grid
+                                        (768, 2048, 4096, 8, 1),      # dW_down grid (1x8)
+                                        (4096, 768, 2048, 8, 8),      # dH grid (8x1)
+                                        (1024, 1024, 1344, 1, 1)])    # one block, 21 stages
+def test_gemm_k64_stages_equal_k32_bit_for_bit(tile, M, N, K, G, Gr):
+    """The 64-K stage kernel adds the same 32-K MFMA steps in the same K
+    order as the 32-K kernel, so C is identical bit for bit; and within
+    the oracle's tolerance."""
+    if (tile == "256x128" and (M // Gr) % 256) or (tile == "128x256" and (N // (G // Gr)) % 256):
+        pytest.skip("tile does not divide the partition")
+    A = W.draw_array(961, M, K, "normal", 1.0)
+    B = W.draw_array(962, K, N, "normal", 0.02)
+    c64 = _run_stage_k(64, A, B, M, N, K, G, Gr, tile)
+    c32 = _run_stage_k(32, A, B, M, N, K, G, Gr, tile)
+    assert np.array_equal(c64, c32)
+    err = OG.errors(OG.decode_bf16(c64), OG.gemm_fp64(A, B))
+    assert err["rel_fro"] <= 5e-3 and err["max_abs"] <= 1e-2 * err["max_ref"]
+
+
+@pytest.mark.parametrize("tile", ["256x128", "128x256", "128x128"])
+@pytest.mark.parametrize("stages", [1, 2, 3, 4, 5, 6, 7, 11, 13, 17, 25])
+def test_gemm_k64_stage_counts(tile, stages):
+    """64-K stage counts that stop inside the lone first steps, the rounds,
+    the loop and the tail of the 3- and 4-stage rings (one chiplet: one K
+    block per operand)."""
+    M, N, K = 256, 256, 64 * stages
+    A = W.draw_array(971 + stages, M, K, "normal", 1.0)
+    B = W.draw_array(972 + stages, K, N, "normal", 0.05)
+    c64 = _run_stage_k(64, A, B, M, N, K, 1, 1, tile)
+    c32 = _run_stage_k(32, A, B, M, N, K, 1, 1, tile)
+    assert np.array_equal(c64, c32)
+    err = OG.errors(OG.decode_bf16(c64), OG.gemm_fp64(A, B))
+    assert err["rel_fro"] <= 5e-3 and err["max_abs"] <= 1e-2 * err["max_ref"]
+
+
 @pytest.mark.parametrize("M,N,K,G,Gr,P,ta,tb", [
     (256, 512, 256, 4, 2, 65536, 0, 0),          # padded strips
     (256, 512, 256, 4, 2, 2 * 1024 * 1024, 0, 1),

@@ -196,3 +196,24 @@ def test_one_workspace_serves_successive_gemms():
         err = OG.errors(C, OG.gemm_fp64(A, B))
         print("errors", err, flush=True)
         assert err["rel_fro"] <= 1e-4
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr,splits", [
+    (768, 2048, 4096, 8, 1, 2),     # 64-K ranges of 32 steps (rounds path)
+    (768, 2048, 4096, 8, 1, 4),     # 16 steps per range
+    (768, 2048, 4096, 8, 1, 5),     # 13 steps per range: per-step path
+    (768, 2048, 4096, 8, 1, 3),     # 32-K ranges of 43 steps: not even, 32-K kernel
+    (4096, 768, 2048, 8, 8, 2),
+])
+def test_splitk_k64_stages_equal_k32_bit_for_bit(M, N, K, G, Gr, splits, monkeypatch):
+    """Where the K ranges are whole 64-K stages, the 64-K stage kernel
+    writes the same partials as the 32-K one (same 32-K MFMA steps, same
+    order), so the reduced C is identical bit for bit."""
+    A = _draw(BF16, 9500 + M + K, M, K)
+    B = _draw(BF16, 9600 + N + K, K, N, "normal", 0.05)
+    C64, r64 = run_splitk(A, B, M, N, K, G, Gr, BF16, FP32, splits)
+    monkeypatch.setenv("CCL_GEMM_STAGE_K", "32")
+    C32, r32 = run_splitk(A, B, M, N, K, G, Gr, BF16, FP32, splits)
+    assert r64 == r32 == splits
+    assert np.array_equal(C64, C32)
+    assert OG.errors(C64, OG.gemm_fp64(A, B))["rel_fro"] <= 1e-4
