@@ -771,8 +771,10 @@ def main():
                                         "path, so an upper bound on HBM bytes"),
                      "algorithmic_bytes": ALGO_BYTES,
                      "traffic_over_algorithmic": (round(traffic / ALGO_BYTES, 3) if traffic else None),
-                     "kernel": "gemm_kernel<256,256,%d waves> (up and down launches)" % (
-                         8 if ccl.ccl_debug_gemm_config(plan_up)[:2] == (256, 256) else 4),
+                     "kernel": ("gemm_kernel<256,256,8 waves> (up and down launches)"
+                                if os.environ.get("CCL_GEMM_A_PAIRS") == "0" else
+                                "gemm_a2_kernel (256x256, 8 waves, A staged in 64-K pairs; up and "
+                                "down launches)"),
                      "avg_launch_ms": round(gemm_ms, 4),
                      "launch_ms": {g: {"mean": round(avg[g], 4), "median": round(float(np.median(per[g])), 4),
                                        "min": round(float(np.min(per[g])), 4)} for g in ("gemm_up", "gemm_down")}},

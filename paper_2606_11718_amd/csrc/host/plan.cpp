@@ -157,6 +157,16 @@ void choose_gemm_config(Plan* p) {
                (p->K / p->Gc) % 64 == 0 && (p->K / p->Gr) % 64 == 0) ? 64 : 32;
   if (const char* e = std::getenv("CCL_GEMM_STAGE_K"))
     if (std::atoi(e) == 32) g.stage_k = 32;
+  // 256x256 keeps 32-K steps for B and the MFMA schedule but stages A in
+  // 64-K pairs of steps: whole 128-byte lines per A load, and loads four
+  // steps ahead in a ring of three pair buffers. Same box, alternating:
+  // 8192x28672x8192 1416-1423 -> 1484-1492 TFLOP/s, 8192x8192x28672
+  // 1433-1437 -> 1504-1508, at the same 1400 W. Needs A's K blocks in
+  // whole pairs. CCL_GEMM_A_PAIRS=0 selects the 32-K A stages.
+  g.a_pairs = p->ab_type == DT_BF16 && g.waves == 8 && btm == 256 && btn == 256 &&
+              (p->K / p->Gc) % 64 == 0;
+  if (const char* e = std::getenv("CCL_GEMM_A_PAIRS"))
+    if (std::atoi(e) == 0) g.a_pairs = false;
   if (g.workgroups > 0x7fffffff) {
     g.why_unsupported = "launch too large";
     return;

@@ -2,9 +2,12 @@
 // III-C: the arithmetic is the plain tiled GEMM; only the operand address
 // map is CCL's).
 //
-// Three kernels share the tile map, the operand descriptors, the
+// The kernels share the tile map, the operand descriptors, the
 // direct-to-LDS loads and the epilogue:
 //  * gemm_kernel: bf16 operands (described below);
+//  * gemm_a2_kernel: bf16 256x256 with A staged in 64-K pairs of steps
+//    (whole-line A loads), otherwise gemm_kernel's schedule;
+//  * gemm_k64_kernel: bf16 tiles below 256x256 with 64-K stages;
 //  * gemm_fp8x_kernel: fp8 operands on 256x256 tiles with 8 waves and K
 //    blocks that are multiples of 128 (v_mfma_f32_16x16x128_f8f6f4);
 //  * gemm_fp8_kernel: the other fp8 plans (v_mfma_f32_32x32x64_f8f6f4).
@@ -35,6 +38,7 @@
 
 #include <cstdint>
 #include <mutex>
+#include <type_traits>
 
 #include "kernels.hpp"
 
@@ -1064,6 +1068,312 @@ __global__ void __launch_bounds__(512, 2) gemm_k64_kernel(GemmParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// bf16 256x256 with whole-line A loads. The 32-K kernel fetches A as 64-byte
+// half lines; here A is staged in 64-K pairs of steps (256 rows of 128
+// bytes, chunk c of row r at c ^ swz_a64(r)), in a ring of three pair
+// buffers (96 KiB), beside B's ring of four 32-K stages (64 KiB). Step s
+// reads A from pair s / 2 (half s % 2) and B from stage s % 4; each step
+// loads B for step s + 3 and every even step loads the A pair of steps
+// s + 4, s + 5, into the buffer its steps s - 2, s - 1 left. A wave issues
+// its A loads before its B loads, so at every stage barrier exactly 8 of
+// its loads may stay in flight (those of the two previous steps' B and the
+// current even step's A, or the previous even step's A and B and the
+// current step's B). The MFMA schedule is the 32-K kernel's.
+// ---------------------------------------------------------------------------
+
+struct TileA2 {
+  static constexpr int BM = 256, BN = 256, WGN = 4;
+  static constexpr int NW = 8;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;     // wave tile 128 x 64
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int A2_BYTES = BM * 128;            // one pair of K steps
+  static constexpr int B_BYTES = kBK * BN * 2;         // one 32-K stage
+  static constexpr int NP = 3;                         // A pair buffers
+  static constexpr int NSB = 4;                        // B stages
+  static constexpr int NAP = A2_BYTES / (1024 * NW);   // A loads per wave per pair
+  static constexpr int CPR_B = BN / 8;
+  static constexpr int RPI_B = 64 / CPR_B;
+  static constexpr int NB = B_BYTES / (1024 * NW);     // B loads per wave per step
+  static_assert(NP * A2_BYTES + NSB * B_BYTES <= 160 * 1024, "LDS exceeds 160 KiB");
+  static_assert(NAP == 4 && NB == 2, "the stage wait count below assumes 4 + 2 loads");
+};
+
+__global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using T = TileA2;
+  constexpr int BM = T::BM, BN = T::BN;
+  __shared__ __attribute__((aligned(1024))) char smA[T::NP][T::A2_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[T::NSB][T::B_BYTES];
+
+  const bool tl_on = p.timeline != nullptr;
+  uint64_t tl_rt[3] = {0, 0, 0}, tl_clk[2] = {0, 0};
+  if (tl_on) {
+    tl_rt[0] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[0] = __builtin_amdgcn_s_memtime();
+  }
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  const int32_t ksteps = p.ksteps;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
+
+  uint32_t a_voff[T::NAP];
+#pragma unroll
+  for (int i = 0; i < T::NAP; ++i) {
+    const int row = 8 * (wave * T::NAP + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz_a64(row);
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
+  }
+  uint32_t b_voff[T::NB];
+#pragma unroll
+  for (int i = 0; i < T::NB; ++i) {
+    const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
+    const int chunk = (lane % T::CPR_B) ^ swz_b(row);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 8) * 2u;
+  }
+  const int32_t a_extent = (BM - 1) * p.a.ld * 2 + 128;
+  const int32_t b_extent = (kBK - 1) * p.b.ld * 2 + BN * 2;
+
+  int32_t a_rd[2];
+  {
+    const int row = wm * T::WM + (lane & 15);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      a_rd[kk] = row * 128 + (((4 * kk + (lane >> 4)) ^ swz_a64(row)) * 16);
+  }
+  int32_t b_rd[T::TN][2];
+  {
+    const int g = lane >> 4, s4 = lane & 15;
+#pragma unroll
+    for (int nt = 0; nt < T::TN; ++nt) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int krow = 8 * g + 4 * r + (s4 >> 2);
+        const int col = wn * T::WN + nt * 16 + 4 * (s4 & 3);
+        b_rd[nt][r] = krow * (BN * 2) + (((col >> 3) ^ swz_b(krow)) * 16) + ((col >> 2) & 1) * 8;
+      }
+    }
+  }
+
+  // ---- operand corners. A advances one pair (64 K) at a time, B one step ----
+  const uint16_t* a_base = p.A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
+  const uint16_t* b_base = p.B + pc * p.b.part + tj * BN;
+  const char* a_next = reinterpret_cast<const char*>(a_base);
+  const char* b_next = reinterpret_cast<const char*>(b_base);
+  const int32_t a_pairs = p.a.kslice / 64, b_steps = p.b.kslice / kBK;
+  int32_t a_left = a_pairs, b_left = b_steps;
+  const int64_t a_adv = 128, b_adv = (int64_t)kBK * p.b.ld * 2;
+  const int64_t a_jump = (p.a.slice - p.a.kslice) * 2;
+  const int64_t b_jump = (p.b.slice - (int64_t)p.b.kslice * p.b.ld) * 2;
+  auto pair_src = [&](bool live) {
+    const i32x4 r = buffer_rsrc(a_next, live ? a_extent : 0);
+    const bool wrap = --a_left == 0;
+    a_next += a_adv + (wrap ? a_jump : 0);
+    a_left = wrap ? a_pairs : a_left;
+    return r;
+  };
+  auto b_src = [&](bool live) {
+    const i32x4 r = buffer_rsrc(b_next, live ? b_extent : 0);
+    const bool wrap = --b_left == 0;
+    b_next += b_adv + (wrap ? b_jump : 0);
+    b_left = wrap ? b_steps : b_left;
+    return r;
+  };
+  const int32_t b_extent4 = (4 * kBK - 1) * p.b.ld * 2 + BN * 2;
+  const uint32_t so_b[4] = {0u, (uint32_t)b_adv, (uint32_t)(2 * b_adv), (uint32_t)(3 * b_adv)};
+  auto b_round_src = [&]() {
+    const i32x4 r = buffer_rsrc(b_next, b_extent4);
+    const bool wrap = b_left == 4;
+    b_next += 4 * b_adv + (wrap ? b_jump : 0);
+    b_left = wrap ? b_steps : b_left - 4;
+    return r;
+  };
+  // Memory op i of a step's first half: A loads (i < NAP, even steps), then
+  // B loads.
+  auto load_a = [&](const i32x4& ra, char* dstA, int i) {
+    lds_dma16(ra, a_voff[i], dstA + (wave * T::NAP + i) * 1024);
+  };
+  auto load_b = [&](const i32x4& rb, int j, char* dstB, int i) {
+    char* dst = dstB + (wave * T::NB + i) * 1024;
+    if (j < 0) lds_dma16(rb, b_voff[i], dst);
+    else lds_dma16_so(rb, b_voff[i], so_b[j], dst);
+  };
+
+  constexpr int kHalfM = T::TM / 2;
+  AFrags<T::TM> fa;
+  BFrags<T::TN> fb0, fb1;
+  auto read_a = [&](const char* sA, int kk, int mt) {
+    fa.a[mt] = *(const lds_bf16x8*)(sA + a_rd[kk] + mt * 16 * 128);
+  };
+  auto read_b = [&](const char* sB, BFrags<T::TN>& fb, int i) {
+    const int nt = i >> 1, r = i & 1;
+    fb.b[nt][r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sB + b_rd[nt][r]));
+  };
+  f32x4 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+  auto mfma_one = [&](const BFrags<T::TN>& fb, int mt, int nt) {
+    const bf16x8 bv = __builtin_bit_cast(
+        bf16x8, __builtin_shufflevector(fb.b[nt][0], fb.b[nt][1], 0, 1, 2, 3, 4, 5, 6, 7));
+    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bv, fa.a[mt], acc[mt][nt], 0, 0, 0);
+  };
+  auto stage_barrier = [&]() {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(8, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // One step: A half kk of pair buffer sA, B stage sB; fragments of the
+  // next step from (nA, nkk) and nB. With LA the step loads the A pair
+  // (descriptor ra) into lA; B loads for step + 3 go to lB.
+  auto step = [&](auto LA, const char* sA, int kk, const char* sB, const BFrags<T::TN>& fb,
+                  BFrags<T::TN>& fbn, char* lA, const i32x4& ra, char* lB, const i32x4& rb, int j,
+                  const char* nA, int nkk, const char* nB) {
+    constexpr bool kLoadA = decltype(LA)::value;
+    constexpr int kMfmaHalf = kHalfM * T::TN;
+    constexpr int kNA = kLoadA ? T::NAP : 0;
+    constexpr int kOps1 = kHalfM + kNA + T::NB;
+#pragma unroll
+    for (int i = 0; i < kMfmaHalf; ++i) {
+      mfma_one(fb, i / T::TN, i % T::TN);
+      if (i < kHalfM) read_a(sA, kk, kHalfM + i);
+      else if (i < kHalfM + kNA) load_a(ra, lA, i - kHalfM);
+      else if (i < kOps1) load_b(rb, j, lB, i - kHalfM - kNA);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfmaHalf; i < kOps1; ++i) {
+      if (i < kHalfM) read_a(sA, kk, kHalfM + i);
+      else if (i < kHalfM + kNA) load_a(ra, lA, i - kHalfM);
+      else load_b(rb, j, lB, i - kHalfM - kNA);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    stage_barrier();
+    constexpr int kOps2 = kHalfM + 2 * T::TN;
+#pragma unroll
+    for (int i = 0; i < kMfmaHalf; ++i) {
+      mfma_one(fb, kHalfM + i / T::TN, i % T::TN);
+      if (i < kHalfM) read_a(nA, nkk, i);
+      else if (i < kOps2) read_b(nB, fbn, i - kHalfM);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = kMfmaHalf; i < kOps2; ++i) {
+      if (i < kHalfM) read_a(nA, nkk, i);
+      else read_b(nB, fbn, i - kHalfM);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Prologue, in the order the steady state issues them: A pair 0, B 0,
+  // A pair 1, B 1, B 2; then A pair 0 and B 0 complete.
+  {
+    const i32x4 r0 = pair_src(0 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NAP; ++i) load_a(r0, smA[0], i);
+    const i32x4 b0 = b_src(0 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NB; ++i) load_b(b0, -1, smB[0], i);
+    const i32x4 r1 = pair_src(2 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NAP; ++i) load_a(r1, smA[1], i);
+    const i32x4 b1 = b_src(1 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NB; ++i) load_b(b1, -1, smB[1], i);
+    const i32x4 b2 = b_src(2 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NB; ++i) load_b(b2, -1, smB[2], i);
+  }
+  stage_barrier();
+  if (tl_on) tl_rt[1] = __builtin_amdgcn_s_memrealtime();
+#pragma unroll
+  for (int mt = 0; mt < kHalfM; ++mt) read_a(smA[0], 0, mt);
+#pragma unroll
+  for (int i = 0; i < 2 * T::TN; ++i) read_b(smB[0], fb0, i);
+
+  // Step s (phase ph = s mod 12): A pair buffer (s / 2) % 3, half s % 2; B
+  // stage s % 4; even steps load the A pair s / 2 + 2 into buffer
+  // (s / 2 + 2) % 3; B loads of step s + 3 into stage (s + 3) % 4.
+  auto phase_step = [&](auto PH, const i32x4& rb, int j, int32_t s) {
+    constexpr int ph = decltype(PH)::value;
+    constexpr bool even = ph % 2 == 0;
+    i32x4 ra = {0, 0, 0, 0};
+    if constexpr (even) ra = pair_src(2 * (s / 2 + 2) < ksteps);
+    step(std::integral_constant<bool, even>{}, smA[(ph / 2) % 3], ph % 2, smB[ph % 4],
+         ph % 2 ? fb1 : fb0, ph % 2 ? fb0 : fb1, smA[(ph / 2 + 2) % 3], ra, smB[(ph + 3) % 4], rb,
+         j, smA[((ph + 1) / 2) % 3], (ph + 1) % 2, smB[(ph + 1) % 4]);
+  };
+  auto single_step = [&](auto PH, int32_t s) {
+    const i32x4 rb = b_src(s + 3 < ksteps);
+    phase_step(PH, rb, -1, s);
+  };
+  int32_t s = 0;
+  if (p.round_fast) {
+    // Step 0 alone; rounds of 4 B-steps (s = 1 mod 4) whose B loads share
+    // one descriptor; 12 steps per loop iteration so that every phase is a
+    // compile-time constant; the remaining steps (at most 14) alone.
+    single_step(std::integral_constant<int, 0>{}, 0);
+    for (s = 1; s + 12 + 3 <= ksteps; s += 12) {
+      const i32x4 rb0 = b_round_src();
+      phase_step(std::integral_constant<int, 1>{}, rb0, 0, s);
+      phase_step(std::integral_constant<int, 2>{}, rb0, 1, s + 1);
+      phase_step(std::integral_constant<int, 3>{}, rb0, 2, s + 2);
+      phase_step(std::integral_constant<int, 4>{}, rb0, 3, s + 3);
+      const i32x4 rb1 = b_round_src();
+      phase_step(std::integral_constant<int, 5>{}, rb1, 0, s + 4);
+      phase_step(std::integral_constant<int, 6>{}, rb1, 1, s + 5);
+      phase_step(std::integral_constant<int, 7>{}, rb1, 2, s + 6);
+      phase_step(std::integral_constant<int, 8>{}, rb1, 3, s + 7);
+      const i32x4 rb2 = b_round_src();
+      phase_step(std::integral_constant<int, 9>{}, rb2, 0, s + 8);
+      phase_step(std::integral_constant<int, 10>{}, rb2, 1, s + 9);
+      phase_step(std::integral_constant<int, 11>{}, rb2, 2, s + 10);
+      phase_step(std::integral_constant<int, 12>{}, rb2, 3, s + 11);
+    }
+#define CCL_A2_TAIL(t) if (s + (t) < ksteps) single_step(std::integral_constant<int, 1 + (t)>{}, s + (t))
+    CCL_A2_TAIL(0); CCL_A2_TAIL(1); CCL_A2_TAIL(2); CCL_A2_TAIL(3); CCL_A2_TAIL(4);
+    CCL_A2_TAIL(5); CCL_A2_TAIL(6); CCL_A2_TAIL(7); CCL_A2_TAIL(8); CCL_A2_TAIL(9);
+    CCL_A2_TAIL(10); CCL_A2_TAIL(11); CCL_A2_TAIL(12); CCL_A2_TAIL(13);
+#undef CCL_A2_TAIL
+  } else {
+    for (; s + 12 <= ksteps; s += 12) {
+#define CCL_A2_STEP(t) single_step(std::integral_constant<int, (t)>{}, s + (t))
+      CCL_A2_STEP(0); CCL_A2_STEP(1); CCL_A2_STEP(2); CCL_A2_STEP(3); CCL_A2_STEP(4); CCL_A2_STEP(5);
+      CCL_A2_STEP(6); CCL_A2_STEP(7); CCL_A2_STEP(8); CCL_A2_STEP(9); CCL_A2_STEP(10); CCL_A2_STEP(11);
+#undef CCL_A2_STEP
+    }
+#define CCL_A2_REST(t) if (s + (t) < ksteps) single_step(std::integral_constant<int, (t)>{}, s + (t))
+    CCL_A2_REST(0); CCL_A2_REST(1); CCL_A2_REST(2); CCL_A2_REST(3); CCL_A2_REST(4); CCL_A2_REST(5);
+    CCL_A2_REST(6); CCL_A2_REST(7); CCL_A2_REST(8); CCL_A2_REST(9); CCL_A2_REST(10);
+#undef CCL_A2_REST
+  }
+
+  if (tl_on) {
+    tl_rt[2] = __builtin_amdgcn_s_memrealtime();
+    tl_clk[1] = __builtin_amdgcn_s_memtime();
+  }
+  static_assert((BM / 2) * BN * 2 <= T::NP * T::A2_BYTES && (BM / 2) * BN * 2 <= T::NSB * T::B_BYTES,
+                "each half of the bf16 C tile fits in one operand's buffers");
+  if (p.epi == 0 && !p.c_f32 && !p.ws)
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
+                                                                 pc, ti, tj, wm, wn, wave, lane);
+  else
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+  if (tl_on) record_timeline(p.timeline + ((int64_t)blockIdx.x * T::NW + wave) * kTimelineWords,
+                             tl_rt, tl_clk, lane);
+#endif
+}
+
+// ---------------------------------------------------------------------------
 // fp8 (E4M3) operands: C = A B with v_mfma_f32_32x32x64_f8f6f4 (unscaled).
 // A K step is 64 fp8 elements, so one stage holds the same bytes as a bf16
 // step (A rows of 64 bytes, B rows of BN bytes x 64 rows) and the A side
@@ -1743,6 +2053,11 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
 #undef CCL_LAUNCH64
       return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
     }
+  }
+  if (g.a_pairs && !fp8 && splits == 1 && waves == 8 && g.tile_m == 256 && g.tile_n == 256 &&
+      a.kslice % 64 == 0) {
+    hipLaunchKernelGGL(gemm_a2_kernel, grid, dim3(TileA2::THREADS), 0, stream, gp);
+    return hipGetLastError();
   }
 #define CCL_LAUNCH(BM_, BN_, WGN_)                                                     \
   hipLaunchKernelGGL((gemm_kernel<BM_, BN_, WGN_>), grid, dim3(Tile<BM_, BN_, WGN_>::THREADS), 0, \

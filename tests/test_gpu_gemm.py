@@ -150,6 +150,31 @@ def test_gemm_k64_stage_counts(tile, stages):
     assert err["rel_fro"] <= 5e-3 and err["max_abs"] <= 1e-2 * err["max_ref"]
 
 
+def _run_a_pairs(on, A, B, M, N, K, G, Gr):
+    os.environ["CCL_GEMM_A_PAIRS"] = "1" if on else "0"
+    try:
+        Cbits, _ = run_gemm(A, 0, B, 0, M, N, K, G, Gr, 4096, "256x256", waves=8)
+    finally:
+        os.environ.pop("CCL_GEMM_A_PAIRS", None)
+    return Cbits
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(512, 512, 64 * k, 1, 1) for k in (1, 2, 3, 4, 5, 7, 8, 9, 13, 14, 15, 22)]
+                         + [(2048, 2048, 2048, 8, 2), (2048, 2048, 4096, 8, 1), (2048, 2048, 2048, 8, 8)])
+def test_gemm_a_pairs_equal_32k_bit_for_bit(M, N, K, G, Gr):
+    """The 256x256 kernel with A staged in 64-K pairs (whole-line loads)
+    adds the same 32-K MFMA steps in the same K order as the 32-K kernel:
+    C is identical bit for bit, for step counts that stop inside the
+    prologue, the rounds, the loop and the tail, and over CCL K blocks."""
+    A = W.draw_array(981 + K, M, K, "normal", 1.0)
+    B = W.draw_array(982 + K, K, N, "normal", 0.05)
+    on = _run_a_pairs(True, A, B, M, N, K, G, Gr)
+    off = _run_a_pairs(False, A, B, M, N, K, G, Gr)
+    assert np.array_equal(on, off)
+    err = OG.errors(OG.decode_bf16(on), OG.gemm_fp64(A, B))
+    assert err["rel_fro"] <= 5e-3 and err["max_abs"] <= 1e-2 * err["max_ref"]
+
+
 @pytest.mark.parametrize("M,N,K,G,Gr,P,ta,tb", [
     (256, 512, 256, 4, 2, 65536, 0, 0),          # padded strips
     (256, 512, 256, 4, 2, 2 * 1024 * 1024, 0, 1),
