@@ -1099,6 +1099,17 @@ struct TileA2 {
   static_assert(NAP == 4 && NB == 2, "the stage wait count below assumes 4 + 2 loads");
 };
 
+// Column tile of the j-th MFMA in tile row mt of a step: the rows are
+// walked in a snake (odd rows right to left), so that consecutive MFMAs of
+// a wave change one operand fragment, never both. Every accumulator still
+// takes its K steps in order (same bits). Same box, alternating processes,
+// 1400 W: +0.3-0.8 % TFLOP/s and a ~10 MHz higher sustained clock on the
+// Llama FFN GEMMs.
+template <int TN>
+__device__ __forceinline__ constexpr int a2_nt(int mt, int j) {
+  return (mt & 1) ? TN - 1 - j : j;
+}
+
 __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)
   using T = TileA2;
@@ -1244,7 +1255,7 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
     constexpr int kOps1 = kHalfM + kNA + T::NB;
 #pragma unroll
     for (int i = 0; i < kMfmaHalf; ++i) {
-      mfma_one(fb, i / T::TN, i % T::TN);
+      mfma_one(fb, i / T::TN, a2_nt<T::TN>(i / T::TN, i % T::TN));
       if (i < kHalfM) read_a(sA, kk, kHalfM + i);
       else if (i < kHalfM + kNA) load_a(ra, lA, i - kHalfM);
       else if (i < kOps1) load_b(rb, j, lB, i - kHalfM - kNA);
@@ -1261,7 +1272,7 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
     constexpr int kOps2 = kHalfM + 2 * T::TN;
 #pragma unroll
     for (int i = 0; i < kMfmaHalf; ++i) {
-      mfma_one(fb, kHalfM + i / T::TN, i % T::TN);
+      mfma_one(fb, kHalfM + i / T::TN, a2_nt<T::TN>(kHalfM + i / T::TN, i % T::TN));
       if (i < kHalfM) read_a(nA, nkk, i);
       else if (i < kOps2) read_b(nB, fbn, i - kHalfM);
       __builtin_amdgcn_sched_barrier(0);
