@@ -167,6 +167,13 @@ void choose_gemm_config(Plan* p) {
               (p->K / p->Gc) % 64 == 0;
   if (const char* e = std::getenv("CCL_GEMM_A_PAIRS"))
     if (std::atoi(e) == 0) g.a_pairs = false;
+  // fp8 256x256 (16x16x128 kernel): three A and two B stage buffers, two
+  // barriers per step, and the next step's fragments read behind the last
+  // rows of MFMAs (gemm_fp8p_kernel). CCL_GEMM_FP8_PIPE=0 selects the
+  // two-stage kernel that reads them after each step's barrier.
+  g.fp8_pipe = p->ab_type == DT_FP8_E4M3 && g.waves == 8 && btm == 256 && btn == 256;
+  if (const char* e = std::getenv("CCL_GEMM_FP8_PIPE"))
+    if (std::atoi(e) == 0) g.fp8_pipe = false;
   if (g.workgroups > 0x7fffffff) {
     g.why_unsupported = "launch too large";
     return;

@@ -48,6 +48,7 @@ struct GemmConfig {
   int waves = 4;                    // waves per workgroup (4 or 8)
   int stage_k = 32;                 // bf16: K extent of one LDS stage (32 or 64)
   bool a_pairs = false;             // bf16 256x256: A staged in 64-K pairs (whole lines)
+  bool fp8_pipe = false;            // fp8 256x256: fragment reads pipelined across steps
   bool supported = false;           // whether ccl_gemm can run this plan
   std::string why_unsupported;
 };

@@ -8,8 +8,11 @@
 //  * gemm_a2_kernel: bf16 256x256 with A staged in 64-K pairs of steps
 //    (whole-line A loads), otherwise gemm_kernel's schedule;
 //  * gemm_k64_kernel: bf16 tiles below 256x256 with 64-K stages;
-//  * gemm_fp8x_kernel: fp8 operands on 256x256 tiles with 8 waves and K
-//    blocks that are multiples of 128 (v_mfma_f32_16x16x128_f8f6f4);
+//  * gemm_fp8p_kernel: fp8 operands on 256x256 tiles with 8 waves and K
+//    blocks that are multiples of 128 (v_mfma_f32_16x16x128_f8f6f4), the
+//    fragment reads pipelined across steps;
+//  * gemm_fp8x_kernel: the same plans with two stages and the fragment reads
+//    after each step's barrier (CCL_GEMM_FP8_PIPE=0);
 //  * gemm_fp8_kernel: the other fp8 plans (v_mfma_f32_32x32x64_f8f6f4).
 //
 // bf16: workgroup = 2 x WGN waves, output tile BM x BN, K step 32 (kBK).
@@ -1883,6 +1886,277 @@ __global__ void __launch_bounds__(128 * WGN, WGN / 2) gemm_fp8x_kernel(GemmParam
 #endif
 }
 
+// ---------------------------------------------------------------------------
+// fp8 256x256 with the fragment reads pipelined across steps
+// (gemm_fp8p_kernel). Same MFMA (16x16x128), K order, fragment layout and
+// swizzles as gemm_fp8x_kernel, so every accumulator takes the same MFMAs
+// in the same order and C is identical bit for bit; what changes is when
+// loads and fragment reads are issued.
+//
+// gemm_fp8x_kernel opens every 128-K step with a barrier that waits for all
+// of the step's loads, then issues the next step's loads and 18 fragment
+// reads before its first MFMA: the matrix cores wait on that at every step.
+// Here A has three 32 KiB stage buffers and B two (160 KiB), and a step
+// (8 rows of 4 MFMAs per wave, snake order) has two barriers:
+//  * after row 0 (X): every wave has read all of stage t's B fragments and
+//    all of stage t-1's A, so the loads of stage t+2 (A into buffer
+//    (t+2) % 3, B into (t+2) % 2) go out in rows 1-2;
+//  * after row 5 (Y): stage t+1 is complete (its loads went out a step
+//    earlier; only stage t+2's may still be in flight), so rows 6-7 read
+//    stage t+1's B fragments (tiles 0-1 into two spare fragments, tiles 3
+//    and 2 into the registers of the current ones right after their last
+//    MFMA) and its A tile 0, behind the MFMAs.
+// The next step's first MFMAs thus find their fragments in registers. The
+// B fragment registers rotate with step parity (the loop runs step pairs).
+// ---------------------------------------------------------------------------
+
+struct TileFp8P {
+  static constexpr int BM = 256, BN = 256, WGN = 4;
+  static constexpr int NW = 8;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WM = BM / 2, WN = BN / WGN;     // wave tile 128 x 64
+  static constexpr int TM = WM / 16, TN = WN / 16;     // 8 x 4 MFMA tiles
+  static constexpr int A_BYTES = BM * kBK8x;           // one stage
+  static constexpr int B_BYTES = kBK8x * BN;
+  static constexpr int NSA = 3, NSB = 2;
+  static constexpr int NA = A_BYTES / (1024 * NW);     // 4 A loads per wave per stage
+  static constexpr int CPR_B = BN / 16;
+  static constexpr int RPI_B = 64 / CPR_B;
+  static constexpr int NB = B_BYTES / (1024 * NW);     // 4 B loads per wave per stage
+  static constexpr int NL = NA + NB;
+  static constexpr int ROW_X = 0, ROW_Y = 5;           // rows followed by a barrier
+  static_assert(NSA * A_BYTES + NSB * B_BYTES <= 160 * 1024, "LDS exceeds 160 KiB");
+  static_assert(TM == 8 && TN == 4, "the row schedule below is written for 8 x 4 MFMA tiles");
+};
+
+__global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using T = TileFp8P;
+  constexpr int BM = T::BM, BN = T::BN;
+  __shared__ __attribute__((aligned(1024))) char smA[T::NSA][T::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smB[T::NSB][T::B_BYTES];
+
+  int32_t pr, pc, ti, tj, split;
+  if (!tile_of_block(p, &pr, &pc, &ti, &tj, &split)) return;
+  const int32_t ksteps = p.ksteps;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
+
+  uint32_t a_voff[T::NA];
+#pragma unroll
+  for (int i = 0; i < T::NA; ++i) {
+    const int row = 8 * (wave * T::NA + i) + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz_a8x(row);
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 16);
+  }
+  uint32_t b_voff[T::NB];
+#pragma unroll
+  for (int i = 0; i < T::NB; ++i) {
+    const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
+    const int chunk = (lane % T::CPR_B) ^ swz_b8x<BN>(row);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 16);
+  }
+  const int32_t a_extent = (BM - 1) * p.a.ld + kBK8x;
+  const int32_t b_extent = (kBK8x - 1) * p.b.ld + BN;
+
+  int32_t a_rd[2];
+  {
+    const int row = wm * T::WM + (lane & 15);
+    const int g = lane >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) a_rd[h] = row * kBK8x + (((4 * h + g) ^ swz_a8x(row)) * 16);
+  }
+  int32_t b_rd[T::TN][4];
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int nt = 0; nt < T::TN; ++nt) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int krow = 64 * (r >> 1) + 16 * g + 8 * (r & 1) + (s >> 1);
+        const int col = wn * T::WN + nt * 16 + 8 * (s & 1);
+        b_rd[nt][r] = krow * BN + (((col >> 4) ^ swz_b8x<BN>(krow)) * 16) + (col & 15);
+      }
+    }
+  }
+
+  const char* A = reinterpret_cast<const char*>(p.A);
+  const char* B = reinterpret_cast<const char*>(p.B);
+  const char* a_next = A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
+  const char* b_next = B + pc * p.b.part + tj * BN;
+  const int32_t a_steps = p.a.kslice / kBK8x, b_steps = p.b.kslice / kBK8x;
+  int32_t a_left = a_steps, b_left = b_steps;
+  const int64_t a_adv = kBK8x, b_adv = (int64_t)kBK8x * p.b.ld;
+  const int64_t a_jump = p.a.slice - p.a.kslice;
+  const int64_t b_jump = p.b.slice - (int64_t)p.b.kslice * p.b.ld;
+  struct StageSrc {
+    i32x4 ra, rb;
+  };
+  auto next_src = [&](bool live) __attribute__((always_inline)) {
+    StageSrc d;
+    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
+    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
+    const bool a_wrap = --a_left == 0;
+    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_left = a_wrap ? a_steps : a_left;
+    const bool b_wrap = --b_left == 0;
+    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_left = b_wrap ? b_steps : b_left;
+    return d;
+  };
+  auto load_one = [&](const StageSrc& d, char* sA, char* sB, int i) __attribute__((always_inline)) {
+    if (i < T::NA)
+      lds_dma16(d.ra, a_voff[i], sA + (wave * T::NA + i) * 1024);
+    else
+      lds_dma16(d.rb, b_voff[i - T::NA], sB + (wave * T::NB + (i - T::NA)) * 1024);
+  };
+
+  i32x8 fa[2];                        // A tile mt in fa[mt % 2]
+  i32x8 F0, F1, F2, F3, S0, S1;       // B fragments: four current, two spare
+  auto read_a = [&](const char* sA, int mt, i32x8& f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const i32x4v v = *(const lds_i32x4*)(sA + a_rd[h] + mt * 16 * kBK8x);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) f[4 * h + q] = v[q];
+    }
+  };
+  auto read_b = [&](const char* sB, int nt, i32x8& f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(sB + b_rd[nt][r]));
+      f[2 * r] = v[0];
+      f[2 * r + 1] = v[1];
+    }
+  };
+
+  f32x4 acc[T::TM][T::TN];
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+  auto mfma = [&](int mt, int nt, const i32x8& b) __attribute__((always_inline)) {
+    acc[mt][nt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, fa[mt & 1], acc[mt][nt], 0, 0,
+                                                                  0, 0, 0, 0);
+  };
+  auto barrier = [&](auto VM) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(decltype(VM)::value, 0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // One step on stage t (A buffer sa, B buffer sb), with the current B
+  // fragments in (b0 .. b3) and the spares (s0, s1); stage t + 1 is in
+  // (na, nb); the loads of stage t + 2 go to (la, lb) with descriptors d.
+  // On return the next step's B fragments are (s0, s1, b2, b3) and its A
+  // tile 0 is in fa[0].
+  auto step = [&](const char* sa, const char* na, const char* nb, char* la, char* lb,
+                  const StageSrc& d, i32x8& b0, i32x8& b1, i32x8& b2, i32x8& b3, i32x8& s0,
+                  i32x8& s1) __attribute__((always_inline)) {
+    // row 0 (nt 0..3), A tile 1 behind it
+    mfma(0, 0, b0);
+    read_a(sa, 1, fa[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(0, 1, b1);
+    mfma(0, 2, b2);
+    mfma(0, 3, b3);
+    __builtin_amdgcn_sched_barrier(0);
+    barrier(std::integral_constant<int, 63>{});                          // X
+    // rows 1-5; the loads of stage t + 2 behind rows 1-2
+#pragma unroll
+    for (int mt = 1; mt <= T::ROW_Y; ++mt) {
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int nt = (mt & 1) ? T::TN - 1 - j : j;
+        mfma(mt, nt, nt == 0 ? b0 : nt == 1 ? b1 : nt == 2 ? b2 : b3);
+        if (j == 0) read_a(sa, mt + 1, fa[(mt + 1) & 1]);
+        if (mt <= 2) load_one(d, la, lb, 4 * (mt - 1) + j);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    barrier(std::integral_constant<int, T::NL>{});                       // Y
+    // row 6 (nt 0..3): A tile 7 and the next step's B tiles 0, 1 (spares)
+    mfma(6, 0, b0);
+    read_a(sa, 7, fa[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(6, 1, b1);
+    read_b(nb, 0, s0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(6, 2, b2);
+    read_b(nb, 1, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(6, 3, b3);
+    __builtin_amdgcn_sched_barrier(0);
+    // row 7 (nt 3..0): the next A tile 0 goes to fa[0] first (LDS reads
+    // complete in order, and the next step's first MFMA needs it); the next
+    // B tiles 3, 2 replace the current ones after their last MFMA
+    mfma(7, 3, b3);
+    read_a(na, 0, fa[0]);
+    read_b(nb, 3, b3);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(7, 2, b2);
+    read_b(nb, 2, b2);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma(7, 1, b1);
+    mfma(7, 0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Prologue: stages 0 and 1 in flight; then stage 0's B fragments and A
+  // tile 0.
+  {
+    const StageSrc d0 = next_src(0 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d0, smA[0], smB[0], i);
+    const StageSrc d1 = next_src(1 < ksteps);
+#pragma unroll
+    for (int i = 0; i < T::NL; ++i) load_one(d1, smA[1], smB[1], i);
+  }
+  barrier(std::integral_constant<int, T::NL>{});
+  read_b(smB[0], 0, F0);
+  read_b(smB[0], 1, F1);
+  read_b(smB[0], 2, F2);
+  read_b(smB[0], 3, F3);
+  read_a(smA[0], 0, fa[0]);
+
+  // Step t (phase ph = t mod 6): A buffer ph % 3, B buffer ph % 2; the loads
+  // of stage t + 2 go to A buffer (ph + 2) % 3 and B buffer ph % 2.
+  auto phase_step = [&](auto PH, int32_t t) __attribute__((always_inline)) {
+    constexpr int ph = decltype(PH)::value;
+    const StageSrc d = next_src(t + 2 < ksteps);
+    if constexpr (ph % 2 == 0)
+      step(smA[ph % 3], smA[(ph + 1) % 3], smB[(ph + 1) % 2], smA[(ph + 2) % 3], smB[ph % 2], d,
+           F0, F1, F2, F3, S0, S1);
+    else
+      step(smA[ph % 3], smA[(ph + 1) % 3], smB[(ph + 1) % 2], smA[(ph + 2) % 3], smB[ph % 2], d,
+           S0, S1, F2, F3, F0, F1);
+  };
+  // One loop over groups of 6 steps, each behind a (uniform) bound check, so
+  // that no loop state outlives the loop.
+#define CCL_FP8P_PHASE(k) \
+  if (t + k < ksteps) phase_step(std::integral_constant<int, k>{}, t + k)
+  for (int32_t t = 0; t < ksteps; t += 6) {
+    CCL_FP8P_PHASE(0); CCL_FP8P_PHASE(1); CCL_FP8P_PHASE(2);
+    CCL_FP8P_PHASE(3); CCL_FP8P_PHASE(4); CCL_FP8P_PHASE(5);
+  }
+#undef CCL_FP8P_PHASE
+
+  static_assert((BM / 2) * BN * 2 <= T::NSA * T::A_BYTES && (BM / 2) * BN * 2 <= T::NSB * T::B_BYTES,
+                "each half of the bf16 C tile fits in one operand's stage buffers");
+  if (p.epi == 0 && !p.c_f32 && !p.ws)
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
+                                                                 pc, ti, tj, wm, wn, wave, lane);
+  else
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+#endif
+}
+
 // Records, per workgroup of the GEMM grid, the XCD it ran on and its tile.
 __global__ void __launch_bounds__(64) dispatch_probe_kernel(TileMap map, int32_t tiles_m,
                                                             int32_t tiles_n, int32_t* out) {
@@ -2012,6 +2286,10 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
       a.kslice % kBK8x == 0 && b.kslice % kBK8x == 0) {
     gp.ksteps = (int32_t)(p.K / kBK8x);
     gp.ksteps_per_split = gp.ksteps;
+    if (g.fp8_pipe) {
+      hipLaunchKernelGGL(gemm_fp8p_kernel, grid, dim3(TileFp8P::THREADS), 0, stream, gp);
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL((gemm_fp8x_kernel<256, 256, 4>), grid, dim3(Tile8x<256, 256, 4>::THREADS), 0,
                        stream, gp);
     return hipGetLastError();

@@ -190,3 +190,36 @@ def test_fp8_rowmajor_baseline(remap, c_type):
         assert err["rel_fro"] <= 1e-4
     else:
         assert OG.within_tolerance(err)
+
+
+def _run_pipe(on, A, B, M, N, K, G, Gr, c_type):
+    os.environ["CCL_GEMM_FP8_PIPE"] = "1" if on else "0"
+    try:
+        _, cbuf, grid = run_fp8(A, B, M, N, K, G, Gr, c_type, tile="256x256", waves=8, unpack=False)
+    finally:
+        os.environ.pop("CCL_GEMM_FP8_PIPE", None)
+    return cbuf, grid
+
+
+@pytest.mark.parametrize("M,N,K,G,Gr", [(512, 512, 128 * s, 1, 1) for s in (1, 2, 3, 4, 5, 6, 7, 8, 11, 13)]
+                         + [(2048, 2048, 1024, 8, 2), (2048, 2048, 2048, 8, 1), (2048, 2048, 2048, 8, 8)])
+@pytest.mark.parametrize("c_type", [ccl.CCL_DT_BF16, ccl.CCL_DT_FP32])
+def test_fp8_pipelined_equals_two_stage_bit_for_bit(M, N, K, G, Gr, c_type):
+    """The pipelined 16x16x128 kernel issues every accumulator's MFMAs in the
+    same K order as the two-stage one, so C is identical bit for bit: for
+    step counts that stop inside the prologue, the first group of six steps
+    and later ones, and over CCL K blocks of 2 and 4 steps; and within the
+    oracle's tolerance."""
+    A = W.draw_array_fp8(8700 + K + Gr, M, K, "normal", 1.0)
+    B = W.draw_array_fp8(8800 + K + Gr, K, N, "normal", 1.0)
+    on, (gr, gc) = _run_pipe(True, A, B, M, N, K, G, Gr, c_type)
+    off, _ = _run_pipe(False, A, B, M, N, K, G, Gr, c_type)
+    assert np.array_equal(on, off)
+    bits = OL.unpack(on, M, N, gr, gc, 4096)
+    C = bits.view(np.float32).astype(np.float64) if c_type == ccl.CCL_DT_FP32 else OG.decode_bf16(bits)
+    err = OG.errors(C, OG.gemm_fp64(A, B))
+    print("errors", err, flush=True)
+    if c_type == ccl.CCL_DT_FP32:
+        assert err["rel_fro"] <= 1e-4
+    else:
+        assert OG.within_tolerance(err)
