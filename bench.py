@@ -397,7 +397,8 @@ def fp8_gemms(reps: int):
                      "frac_of_fp8_peak": round(tf / PEAK_FP8_TFLOPS, 4)}
         del A, B, C
     out["peak"] = PEAK_FP8_TFLOPS
-    out["kernel"] = "gemm_fp8x_kernel<256,256,8 waves>, v_mfma_f32_16x16x128_f8f6f4, 128-wide K steps, 2 LDS stages"
+    out["kernel"] = ("gemm_fp8p_kernel (256x256, 8 waves, v_mfma_f32_16x16x128_f8f6f4, 128-wide K "
+                     "steps, 3 A and 2 B LDS stages, fragment reads pipelined across steps)")
     return out
 
 
