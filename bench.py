@@ -454,66 +454,86 @@ def pack_hbm(reps: int):
     return out
 
 
+# One GPU's share of the Llama-3.1-70B FFN under 8-way tensor parallelism:
+# the up projection split by output columns (W_up 8192 x 28672/8), the down
+# projection by its K (W_down 28672/8 x 8192), each GEMM at full token
+# count. The path would shard this way over 8 GPUs; one GPU runs its share.
+TP8_SHARDS = (("llama_up_tp8_shard", 8192, 28672 // 8, 8192),
+              ("llama_down_tp8_shard", 8192, 8192, 28672 // 8))
+
+
+def _time_ccl_and_vendor(name, M, N, K, G, grid_rows, reps):
+    """ccl_gemm on random operands already in CCL (plan at grid_rows, 4 KB
+    pages) and torch.matmul of row-major operands of the same shape, each
+    timed as reps back-to-back launches after 3 warm-up ones; plus the
+    library's split-K choice where it takes more than one range."""
+    import torch
+    from paper_2606_11718_amd import ccl
+
+    flops = 2 * M * N * K
+    plan = ccl.ccl_plan(M, N, K, G, grid_rows, 4096)
+    gr, gc = ccl.ccl_plan_grid(plan)
+    lay = [ccl.ccl_plan_layout(plan, op) for op in (ccl.CCL_A, ccl.CCL_B, ccl.CCL_C)]
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    A = torch.randn(lay[0].total_bytes // 2, device="cuda", generator=gen).to(torch.bfloat16)
+    B = (torch.randn(lay[1].total_bytes // 2, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    C = torch.empty(lay[2].total_bytes // 2, device="cuda", dtype=torch.bfloat16)
+    st = torch.cuda.current_stream()
+
+    def timed(call):
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
+        e0.record(st)
+        for _ in range(reps):
+            call()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    ms = timed(lambda: ccl.ccl_gemm(plan, A, B, C, st))
+    tm, tn, _ = ccl.ccl_debug_gemm_config(plan)
+    rec = {"MNK": f"{M}x{N}x{K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
+           "ms": round(ms, 4), "tflops": round(flops / ms / 1e9, 1)}
+    # the vendor library on the same shape, box and power limit:
+    # torch.matmul of contiguous row-major bf16 operands
+    Ar = torch.randn(M, K, device="cuda", generator=gen).to(torch.bfloat16)
+    Br = (torch.randn(K, N, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    Cr = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+    ms_v = timed(lambda: torch.matmul(Ar, Br, out=Cr))
+    rec["vendor_matmul"] = {"ms": round(ms_v, 4), "tflops": round(flops / ms_v / 1e9, 1),
+                            "ccl_speedup": round(ms_v / ms, 3),
+                            "blas": str(torch.backends.cuda.preferred_blas_library())}
+    del Ar, Br, Cr
+    ranges, ws_bytes = ccl.ccl_gemm_splitk_workspace(plan, 0)
+    if ranges > 1:             # the library's split-K choice for this shape
+        ws = torch.empty(ws_bytes, device="cuda", dtype=torch.uint8)
+        ms_s = timed(lambda: ccl.ccl_gemm_splitk(plan, 1.0, A, B, 0.0, C, ranges, ws,
+                                                 ws_bytes, st))
+        rec["splitk"] = {"ranges": ranges, "ms": round(ms_s, 4),
+                         "tflops": round(flops / ms_s / 1e9, 1)}
+        del ws
+    del A, B, C
+    return rec
+
+
 def workload_gemms(reps: int):
     """Per-launch time of ccl_gemm on every workload GEMM shape (bf16, random
     operands already in CCL), at the grid the parity tests use: the small
-    Qwen3 shapes, the tiny case and the Llama backward GEMMs. Beside each,
-    torch.matmul of row-major operands of the same shape (the vendor BLAS,
-    free to use every CU) timed the same way."""
-    import numpy as np
-    import torch
+    Qwen3 shapes, the tiny case and the Llama backward GEMMs; then one GPU's
+    share of the Llama FFN under 8-way tensor parallelism (TP8_SHARDS, the
+    plan's automatic grid). Beside each, torch.matmul of row-major operands
+    of the same shape (the vendor BLAS, free to use every CU) timed the same
+    way."""
     import workloads as W
-    from paper_2606_11718_amd import ccl
 
     out = {}
     for wl in W.WORKLOADS.values():
         for g in wl.gemms:
-            gr_req = g.grids[0]
-            plan = ccl.ccl_plan(g.M, g.N, g.K, g.chiplets, gr_req, 4096)
-            gr, gc = ccl.ccl_plan_grid(plan)
-            lay = [ccl.ccl_plan_layout(plan, op) for op in (ccl.CCL_A, ccl.CCL_B, ccl.CCL_C)]
-            gen = torch.Generator(device="cuda").manual_seed(5)
-            A = torch.randn(lay[0].total_bytes // 2, device="cuda", generator=gen).to(torch.bfloat16)
-            B = (torch.randn(lay[1].total_bytes // 2, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
-            C = torch.empty(lay[2].total_bytes // 2, device="cuda", dtype=torch.bfloat16)
-            st = torch.cuda.current_stream()
-
-            def timed(call):
-                for _ in range(3):
-                    call()
-                torch.cuda.synchronize()
-                e0, e1 = torch.cuda.Event(True), torch.cuda.Event(True)
-                e0.record(st)
-                for _ in range(reps):
-                    call()
-                e1.record(st)
-                torch.cuda.synchronize()
-                return e0.elapsed_time(e1) / reps
-
-            ms = timed(lambda: ccl.ccl_gemm(plan, A, B, C, st))
-            tm, tn, _ = ccl.ccl_debug_gemm_config(plan)
-            rec = {"MNK": f"{g.M}x{g.N}x{g.K}", "grid": f"{gr}x{gc}", "tile": f"{tm}x{tn}",
-                   "ms": round(ms, 4), "tflops": round(g.flops / ms / 1e9, 1)}
-            # the vendor library on the same shape, box and power limit:
-            # torch.matmul of contiguous row-major bf16 operands
-            Ar = torch.randn(g.M, g.K, device="cuda", generator=gen).to(torch.bfloat16)
-            Br = (torch.randn(g.K, g.N, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
-            Cr = torch.empty(g.M, g.N, device="cuda", dtype=torch.bfloat16)
-            ms_v = timed(lambda: torch.matmul(Ar, Br, out=Cr))
-            rec["vendor_matmul"] = {"ms": round(ms_v, 4), "tflops": round(g.flops / ms_v / 1e9, 1),
-                                    "ccl_speedup": round(ms_v / ms, 3),
-                                    "blas": str(torch.backends.cuda.preferred_blas_library())}
-            del Ar, Br, Cr
-            ranges, ws_bytes = ccl.ccl_gemm_splitk_workspace(plan, 0)
-            if ranges > 1:             # the library's split-K choice for this shape
-                ws = torch.empty(ws_bytes, device="cuda", dtype=torch.uint8)
-                ms_s = timed(lambda: ccl.ccl_gemm_splitk(plan, 1.0, A, B, 0.0, C, ranges, ws,
-                                                         ws_bytes, st))
-                rec["splitk"] = {"ranges": ranges, "ms": round(ms_s, 4),
-                                 "tflops": round(g.flops / ms_s / 1e9, 1)}
-                del ws
-            out[g.name] = rec
-            del A, B, C
+            out[g.name] = _time_ccl_and_vendor(g.name, g.M, g.N, g.K, g.chiplets, g.grids[0], reps)
+    for name, M, N, K in TP8_SHARDS:
+        out[name] = _time_ccl_and_vendor(name, M, N, K, 8, 0, reps)
     return out
 
 

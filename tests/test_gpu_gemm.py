@@ -286,3 +286,20 @@ def test_gemm_rowmajor_baseline(remap, M, N, K, G, Gr):
     got = OG.decode_bf16(from_dev(C).reshape(M, N))
     err = OG.errors(got, OG.gemm_fp64(A, B))
     assert OG.within_tolerance(err), err
+
+
+@pytest.mark.parametrize("M,N,K", [(8192, 28672 // 8, 8192), (8192, 8192, 28672 // 8)])
+def test_gemm_tensor_parallel_shard_full_compare(M, N, K):
+    """One GPU's share of the Llama-3.1-70B FFN under 8-way tensor
+    parallelism (up by output columns, down by K), on the plan's automatic
+    grid: every element of C against the fp64 oracle, in row blocks."""
+    A = W.draw_array(7600 + N, M, K, "normal", 1.0)
+    B = W.draw_array(7700 + K, K, N, "normal", 0.02)
+    (cbuf, gr, gc), _ = run_gemm(A, 0, B, 0, M, N, K, 8, 0, 4096, unpack=False)
+    B_d = OG.decode(B)
+    err = compare_in_row_blocks({0: (cbuf, gr, gc)}, M, N, 4096,
+                                lambda r0, r1: OG.gemm_fp64(OG.decode(A[r0:r1]), B_d),
+                                OG.decode_bf16)[0]
+    print("tp8 shard", M, N, K, "grid", gr, gc, "errors over all of C", err, flush=True)
+    assert err["rel_fro"] <= 5e-3
+    assert err["max_abs"] <= 1e-2 * err["max_ref"]

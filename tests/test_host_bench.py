@@ -66,3 +66,19 @@ def test_committed_traffic_is_dropped_when_the_code_differs(tmp_path, monkeypatc
 @pytest.mark.parametrize("src", bench.GEMM_SRCS)
 def test_hashed_sources_exist(src):
     assert os.path.exists(src)
+
+
+def test_tensor_parallel_shards_are_one_gpus_share_of_the_llama_ffn():
+    """The workload leg's 8-way tensor-parallel shards: the up projection by
+    output columns, the down projection by K; both plan (automatic grid) on
+    whole 256x256 tiles of the 8 XCD partitions."""
+    from paper_2606_11718_amd import ccl
+    shapes = {name: (M, N, K) for name, M, N, K in bench.TP8_SHARDS}
+    assert shapes == {"llama_up_tp8_shard": (8192, 3584, 8192),
+                      "llama_down_tp8_shard": (8192, 8192, 3584)}
+    for M, N, K in shapes.values():
+        p = ccl.ccl_plan(M, N, K, 8, 0, 4096)
+        tm, tn, wgs = ccl.ccl_debug_gemm_config(p)
+        gr, gc = ccl.ccl_plan_grid(p)
+        assert (tm, tn) == (256, 256) and gr * gc == 8
+        assert wgs == 8 * (M // gr // 256) * (N // gc // 256)     # one partition per XCD
