@@ -257,10 +257,16 @@ __global__ void __launch_bounds__(256) pack_trans_reg_kernel(TransArgs a, int32_
   typedef E ev __attribute__((ext_vector_type(EPC)));
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int32_t wcb = blockIdx.x * 4 + wave;
+  // Row block by of column group bx: blockIdx.y skewed by 8 blocks per
+  // column group, so that the workgroups resident at one time read chunks
+  // spread over the whole width of the stored rows instead of one 8 KiB
+  // band of them (a bijection for each bx). Measured on the 134 MB X^T
+  // from HBM: +1-2 %; on the 470 MB W_up^T +0.5 %.
+  const int32_t bx = blockIdx.x, by = (int32_t)((blockIdx.y + blockIdx.x * 8u) % gridDim.y);
+  const int32_t wcb = bx * 4 + wave;
   if (wcb >= wb_cols) return;
   const int la = lane & 7, lb = lane >> 3;
-  const int64_t R0 = (int64_t)blockIdx.y * WB, C0 = (int64_t)wcb * WB;
+  const int64_t R0 = (int64_t)by * WB, C0 = (int64_t)wcb * WB;
   const E* src = reinterpret_cast<const E*>(a.src) + (C0 + EPC * lb) * a.ld + R0 + EPC * la;
   ev in[EPC];
 #pragma unroll
