@@ -146,6 +146,25 @@ __device__ __forceinline__ void lds_dma16_so(i32x4 rsrc, uint32_t voff, uint32_t
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :: "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "m0");
 }
+// A run of loads that share one M0: the first sets M0 to the LDS
+// destination of the run, the next ones (lds_dma16_next<OFF>) reuse it.
+// Their instruction offset moves both the memory address and the LDS
+// destination by OFF bytes (the scalar offset moves the memory address
+// only), so load i of a run lands OFF = 1024 i bytes after the first when
+// its per-lane offset is the plain one minus OFF. The run's loads are
+// volatile asm, kept in order, and nothing between them writes M0.
+__device__ __forceinline__ void lds_dma16_first(i32x4 rsrc, uint32_t voff, uint32_t soff,
+                                                const char* lds) {
+  const uint32_t m0v = (uint32_t)(uintptr_t)(const lds_char*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(m0v), "v"(voff), "s"(rsrc), "s"(soff) : "m0");
+}
+template <int OFF>
+__device__ __forceinline__ void lds_dma16_next(i32x4 rsrc, uint32_t voff, uint32_t soff) {
+  static_assert(OFF > 0 && OFF < 4096, "12-bit instruction offset");
+  asm volatile("buffer_load_dwordx4 %0, %1, %2 offen offset:%3 lds"
+               :: "v"(voff), "s"(rsrc), "s"(soff), "n"(OFF));
+}
 #pragma clang diagnostic pop
 
 // s_waitcnt immediate: vmcnt(vm) and lgkmcnt(lgkm), expcnt not waited on.
@@ -1140,16 +1159,22 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   for (int i = 0; i < T::NAP; ++i) {
     const int row = 8 * (wave * T::NAP + i) + (lane >> 3);
     const int chunk = (lane & 7) ^ swz_a64(row);
-    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u;
+    // minus the instruction offset 1024 i of load i in its run (row >= 8 i
+    // and ld >= 64, so the difference stays non-negative)
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 8) * 2u - 1024u * i;
   }
   uint32_t b_voff[T::NB];
 #pragma unroll
   for (int i = 0; i < T::NB; ++i) {
     const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
     const int chunk = (lane % T::CPR_B) ^ swz_b(row);
-    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 8) * 2u;
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 8) * 2u - 1024u * i;   // row >= 2 i, ld >= 256
   }
-  const int32_t a_extent = (BM - 1) * p.a.ld * 2 + 128;
+  // A: one descriptor for the tile's 256 rows over all K blocks of the
+  // operand (the launch checks that it fits in 31 bits); the scalar offset
+  // selects the pair.
+  const int32_t a_blocks = p.ksteps * kBK / p.a.kslice;
+  const int32_t a_extent = (a_blocks - 1) * p.a.slice * 2 + (BM - 1) * p.a.ld * 2 + p.a.kslice * 2;
   const int32_t b_extent = (kBK - 1) * p.b.ld * 2 + BN * 2;
 
   int32_t a_rd[2];
@@ -1176,19 +1201,31 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   // ---- operand corners. A advances one pair (64 K) at a time, B one step ----
   const uint16_t* a_base = p.A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
   const uint16_t* b_base = p.B + pc * p.b.part + tj * BN;
-  const char* a_next = reinterpret_cast<const char*>(a_base);
   const char* b_next = reinterpret_cast<const char*>(b_base);
   const int32_t a_pairs = p.a.kslice / 64, b_steps = p.b.kslice / kBK;
   int32_t a_left = a_pairs, b_left = b_steps;
-  const int64_t a_adv = 128, b_adv = (int64_t)kBK * p.b.ld * 2;
-  const int64_t a_jump = (p.a.slice - p.a.kslice) * 2;
+  // scalar offset from one pair to the next, and from the last pair of a K
+  // block to the first of the next
+  const uint32_t a_adv = 128u, a_adv_wrap = 128u + (uint32_t)(p.a.slice - p.a.kslice) * 2u;
+  const int64_t b_adv = (int64_t)kBK * p.b.ld * 2;
   const int64_t b_jump = (p.b.slice - (int64_t)p.b.kslice * p.b.ld) * 2;
+  const i32x4 a_desc = buffer_rsrc(a_base, a_extent);
+  uint32_t a_so = 0;
+  struct PairSrc {
+    i32x4 r;
+    uint32_t so;
+  };
+  // The next pair: the descriptor (empty past the last step, so no memory
+  // is touched) and the pair's byte offset from the tile's first row.
   auto pair_src = [&](bool live) {
-    const i32x4 r = buffer_rsrc(a_next, live ? a_extent : 0);
+    PairSrc d;
+    d.r = a_desc;
+    if (!live) d.r[2] = 0;
+    d.so = a_so;
     const bool wrap = --a_left == 0;
-    a_next += a_adv + (wrap ? a_jump : 0);
+    a_so += wrap ? a_adv_wrap : a_adv;
     a_left = wrap ? a_pairs : a_left;
-    return r;
+    return d;
   };
   auto b_src = [&](bool live) {
     const i32x4 r = buffer_rsrc(b_next, live ? b_extent : 0);
@@ -1207,14 +1244,18 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
     return r;
   };
   // Memory op i of a step's first half: A loads (i < NAP, even steps), then
-  // B loads.
-  auto load_a = [&](const i32x4& ra, char* dstA, int i) {
-    lds_dma16(ra, a_voff[i], dstA + (wave * T::NAP + i) * 1024);
+  // B loads. A wave's loads of one operand in one step form a run sharing
+  // M0 (LDS rows 1 KiB apart, 1024 i in the instruction offset).
+  auto load_a = [&](const PairSrc& ra, char* dstA, int i) {
+    if (i == 0) lds_dma16_first(ra.r, a_voff[0], ra.so, dstA + wave * T::NAP * 1024);
+    else if (i == 1) lds_dma16_next<1024>(ra.r, a_voff[1], ra.so);
+    else if (i == 2) lds_dma16_next<2048>(ra.r, a_voff[2], ra.so);
+    else lds_dma16_next<3072>(ra.r, a_voff[3], ra.so);
   };
   auto load_b = [&](const i32x4& rb, int j, char* dstB, int i) {
-    char* dst = dstB + (wave * T::NB + i) * 1024;
-    if (j < 0) lds_dma16(rb, b_voff[i], dst);
-    else lds_dma16_so(rb, b_voff[i], so_b[j], dst);
+    const uint32_t so = j < 0 ? 0u : so_b[j];
+    if (i == 0) lds_dma16_first(rb, b_voff[0], so, dstB + wave * T::NB * 1024);
+    else lds_dma16_next<1024>(rb, b_voff[1], so);
   };
 
   constexpr int kHalfM = T::TM / 2;
@@ -1250,7 +1291,7 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   // next step from (nA, nkk) and nB. With LA the step loads the A pair
   // (descriptor ra) into lA; B loads for step + 3 go to lB.
   auto step = [&](auto LA, const char* sA, int kk, const char* sB, const BFrags<T::TN>& fb,
-                  BFrags<T::TN>& fbn, char* lA, const i32x4& ra, char* lB, const i32x4& rb, int j,
+                  BFrags<T::TN>& fbn, char* lA, const PairSrc& ra, char* lB, const i32x4& rb, int j,
                   const char* nA, int nkk, const char* nB) {
     constexpr bool kLoadA = decltype(LA)::value;
     constexpr int kMfmaHalf = kHalfM * T::TN;
@@ -1291,13 +1332,13 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   // Prologue, in the order the steady state issues them: A pair 0, B 0,
   // A pair 1, B 1, B 2; then A pair 0 and B 0 complete.
   {
-    const i32x4 r0 = pair_src(0 < ksteps);
+    const PairSrc r0 = pair_src(0 < ksteps);
 #pragma unroll
     for (int i = 0; i < T::NAP; ++i) load_a(r0, smA[0], i);
     const i32x4 b0 = b_src(0 < ksteps);
 #pragma unroll
     for (int i = 0; i < T::NB; ++i) load_b(b0, -1, smB[0], i);
-    const i32x4 r1 = pair_src(2 < ksteps);
+    const PairSrc r1 = pair_src(2 < ksteps);
 #pragma unroll
     for (int i = 0; i < T::NAP; ++i) load_a(r1, smA[1], i);
     const i32x4 b1 = b_src(1 < ksteps);
@@ -1320,8 +1361,9 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   auto phase_step = [&](auto PH, const i32x4& rb, int j, int32_t s) {
     constexpr int ph = decltype(PH)::value;
     constexpr bool even = ph % 2 == 0;
-    i32x4 ra = {0, 0, 0, 0};
-    if constexpr (even) ra = pair_src(2 * (s / 2 + 2) < ksteps);
+    // inside the rounds loop (j >= 0) every pair it loads is live
+    PairSrc ra = {};
+    if constexpr (even) ra = pair_src(j >= 0 || 2 * (s / 2 + 2) < ksteps);
     step(std::integral_constant<bool, even>{}, smA[(ph / 2) % 3], ph % 2, smB[ph % 4],
          ph % 2 ? fb1 : fb0, ph % 2 ? fb0 : fb1, smA[(ph / 2 + 2) % 3], ra, smB[(ph + 3) % 4], rb,
          j, smA[((ph + 1) / 2) % 3], (ph + 1) % 2, smB[(ph + 1) % 4]);
@@ -1334,9 +1376,11 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
   if (p.round_fast) {
     // Step 0 alone; rounds of 4 B-steps (s = 1 mod 4) whose B loads share
     // one descriptor; 12 steps per loop iteration so that every phase is a
-    // compile-time constant; the remaining steps (at most 14) alone.
+    // compile-time constant, each loading only live A pairs (the last, at
+    // step s + 11, covers steps s + 15 and s + 16) and B stages; the
+    // remaining steps (at most 15) alone.
     single_step(std::integral_constant<int, 0>{}, 0);
-    for (s = 1; s + 12 + 3 <= ksteps; s += 12) {
+    for (s = 1; s + 16 <= ksteps; s += 12) {
       const i32x4 rb0 = b_round_src();
       phase_step(std::integral_constant<int, 1>{}, rb0, 0, s);
       phase_step(std::integral_constant<int, 2>{}, rb0, 1, s + 1);
@@ -1356,7 +1400,7 @@ __global__ void __launch_bounds__(512, 2) gemm_a2_kernel(GemmParams p) {
 #define CCL_A2_TAIL(t) if (s + (t) < ksteps) single_step(std::integral_constant<int, 1 + (t)>{}, s + (t))
     CCL_A2_TAIL(0); CCL_A2_TAIL(1); CCL_A2_TAIL(2); CCL_A2_TAIL(3); CCL_A2_TAIL(4);
     CCL_A2_TAIL(5); CCL_A2_TAIL(6); CCL_A2_TAIL(7); CCL_A2_TAIL(8); CCL_A2_TAIL(9);
-    CCL_A2_TAIL(10); CCL_A2_TAIL(11); CCL_A2_TAIL(12); CCL_A2_TAIL(13);
+    CCL_A2_TAIL(10); CCL_A2_TAIL(11); CCL_A2_TAIL(12); CCL_A2_TAIL(13); CCL_A2_TAIL(14);
 #undef CCL_A2_TAIL
   } else {
     for (; s + 12 <= ksteps; s += 12) {
@@ -2343,8 +2387,11 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
       return splits > 1 ? launch_splitk_reduce(p, gp, stream) : hipGetLastError();
     }
   }
+  // The 64-K-pair kernel's A descriptor spans the tile's 256 rows over all
+  // K blocks of A.
   if (g.a_pairs && !fp8 && splits == 1 && waves == 8 && g.tile_m == 256 && g.tile_n == 256 &&
-      a.kslice % 64 == 0) {
+      a.kslice % 64 == 0 &&
+      (p.K / a.kslice - 1) * a.slice * 2 + 256 * (int64_t)a.ld * 2 + 4096 < ((int64_t)1 << 31)) {
     hipLaunchKernelGGL(gemm_a2_kernel, grid, dim3(TileA2::THREADS), 0, stream, gp);
     return hipGetLastError();
   }
