@@ -257,12 +257,14 @@ __global__ void __launch_bounds__(256) pack_trans_reg_kernel(TransArgs a, int32_
   typedef E ev __attribute__((ext_vector_type(EPC)));
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  // Row block by of column group bx: blockIdx.y skewed by 8 blocks per
+  // Row block by of column group bx: blockIdx.y skewed by 2 blocks per
   // column group, so that the workgroups resident at one time read chunks
-  // spread over the whole width of the stored rows instead of one 8 KiB
-  // band of them (a bijection for each bx). Measured on the 134 MB X^T
-  // from HBM: +1-2 %; on the 470 MB W_up^T +0.5 %.
-  const int32_t bx = blockIdx.x, by = (int32_t)((blockIdx.y + blockIdx.x * 8u) % gridDim.y);
+  // spread over the width of the stored rows instead of one 8 KiB band of
+  // them (a bijection for each bx). Measured from HBM against no skew:
+  // 134 MB X^T 0.663-0.666 of 8 TB/s against 0.627-0.628, 470 MB W_up^T
+  // 0.710 against 0.698-0.699; skews of 1, 3 and 4 were 0-1 % slower, 8
+  // and 16 (several column groups then share a band) 4 % and 20 % slower.
+  const int32_t bx = blockIdx.x, by = (int32_t)((blockIdx.y + blockIdx.x * 2u) % gridDim.y);
   const int32_t wcb = bx * 4 + wave;
   if (wcb >= wb_cols) return;
   const int la = lane & 7, lb = lane >> 3;
