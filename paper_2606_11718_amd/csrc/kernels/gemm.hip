@@ -1994,17 +1994,24 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
   for (int i = 0; i < T::NA; ++i) {
     const int row = 8 * (wave * T::NA + i) + (lane >> 3);
     const int chunk = (lane & 7) ^ swz_a8x(row);
-    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 16);
+    // minus the instruction offset 1024 i of load i in its run (row >= 8 i,
+    // ld >= 128)
+    a_voff[i] = (uint32_t)(row * p.a.ld + chunk * 16) - 1024u * i;
   }
   uint32_t b_voff[T::NB];
 #pragma unroll
   for (int i = 0; i < T::NB; ++i) {
     const int row = T::RPI_B * (wave * T::NB + i) + lane / T::CPR_B;
     const int chunk = (lane % T::CPR_B) ^ swz_b8x<BN>(row);
-    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 16);
+    b_voff[i] = (uint32_t)(row * p.b.ld + chunk * 16) - 1024u * i;   // row >= 4 i, ld >= 256
   }
-  const int32_t a_extent = (BM - 1) * p.a.ld + kBK8x;
-  const int32_t b_extent = (kBK8x - 1) * p.b.ld + BN;
+  // One descriptor per operand for the whole tile: A's 256 rows and B's
+  // 256 columns over all K blocks (the launch checks that both extents fit
+  // in 31 bits); a stage is selected by the loads' scalar offset.
+  const int32_t K = p.ksteps * kBK8x;
+  const int32_t a_extent = (K / p.a.kslice - 1) * p.a.slice + (BM - 1) * p.a.ld + p.a.kslice;
+  const int32_t b_extent = (int32_t)((K / p.b.kslice - 1) * p.b.slice +
+                                     (int64_t)(p.b.kslice - 1) * p.b.ld + BN);
 
   int32_t a_rd[2];
   {
@@ -2029,34 +2036,50 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
 
   const char* A = reinterpret_cast<const char*>(p.A);
   const char* B = reinterpret_cast<const char*>(p.B);
-  const char* a_next = A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld;
-  const char* b_next = B + pc * p.b.part + tj * BN;
+  const i32x4 a_desc = buffer_rsrc(A + pr * p.a.part + (int64_t)(ti * BM) * p.a.ld, a_extent);
+  const i32x4 b_desc = buffer_rsrc(B + pc * p.b.part + tj * BN, b_extent);
   const int32_t a_steps = p.a.kslice / kBK8x, b_steps = p.b.kslice / kBK8x;
   int32_t a_left = a_steps, b_left = b_steps;
-  const int64_t a_adv = kBK8x, b_adv = (int64_t)kBK8x * p.b.ld;
-  const int64_t a_jump = p.a.slice - p.a.kslice;
-  const int64_t b_jump = p.b.slice - (int64_t)p.b.kslice * p.b.ld;
+  // scalar offsets from one stage to the next, and from the last stage of a
+  // K block to the first of the next
+  const uint32_t a_adv = kBK8x, a_adv_wrap = (uint32_t)(kBK8x + p.a.slice - p.a.kslice);
+  const uint32_t b_adv = (uint32_t)(kBK8x * p.b.ld);
+  const uint32_t b_adv_wrap = (uint32_t)(b_adv + p.b.slice - (int64_t)p.b.kslice * p.b.ld);
+  uint32_t a_so = 0, b_so = 0;
   struct StageSrc {
     i32x4 ra, rb;
+    uint32_t sa, sb;
   };
+  // The next stage: the descriptors (empty past the last step, so no memory
+  // is touched) and the stage's byte offsets.
   auto next_src = [&](bool live) __attribute__((always_inline)) {
     StageSrc d;
-    d.ra = buffer_rsrc(a_next, live ? a_extent : 0);
-    d.rb = buffer_rsrc(b_next, live ? b_extent : 0);
+    d.ra = a_desc;
+    d.rb = b_desc;
+    if (!live) d.ra[2] = d.rb[2] = 0;
+    d.sa = a_so;
+    d.sb = b_so;
     const bool a_wrap = --a_left == 0;
-    a_next += a_adv + (a_wrap ? a_jump : 0);
+    a_so += a_wrap ? a_adv_wrap : a_adv;
     a_left = a_wrap ? a_steps : a_left;
     const bool b_wrap = --b_left == 0;
-    b_next += b_adv + (b_wrap ? b_jump : 0);
+    b_so += b_wrap ? b_adv_wrap : b_adv;
     b_left = b_wrap ? b_steps : b_left;
     return d;
   };
+  // A wave's loads of one operand in one stage form a run sharing one M0
+  // write (LDS rows 1 KiB apart, 1024 i in the instruction offset).
   auto load_one = [&](const StageSrc& d, char* sA, char* sB, int i) __attribute__((always_inline)) {
-    if (i < T::NA)
-      lds_dma16(d.ra, a_voff[i], sA + (wave * T::NA + i) * 1024);
-    else
-      lds_dma16(d.rb, b_voff[i - T::NA], sB + (wave * T::NB + (i - T::NA)) * 1024);
+    if (i == 0) lds_dma16_first(d.ra, a_voff[0], d.sa, sA + wave * T::NA * 1024);
+    else if (i == 1) lds_dma16_next<1024>(d.ra, a_voff[1], d.sa);
+    else if (i == 2) lds_dma16_next<2048>(d.ra, a_voff[2], d.sa);
+    else if (i == 3) lds_dma16_next<3072>(d.ra, a_voff[3], d.sa);
+    else if (i == 4) lds_dma16_first(d.rb, b_voff[0], d.sb, sB + wave * T::NB * 1024);
+    else if (i == 5) lds_dma16_next<1024>(d.rb, b_voff[1], d.sb);
+    else if (i == 6) lds_dma16_next<2048>(d.rb, b_voff[2], d.sb);
+    else lds_dma16_next<3072>(d.rb, b_voff[3], d.sb);
   };
+  static_assert(T::NA == 4 && T::NB == 4, "load runs of 4 per operand and stage");
 
   i32x8 fa[2];                        // A tile mt in fa[mt % 2]
   i32x8 F0, F1, F2, F3, S0, S1;       // B fragments: four current, two spare
@@ -2171,9 +2194,9 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
 
   // Step t (phase ph = t mod 6): A buffer ph % 3, B buffer ph % 2; the loads
   // of stage t + 2 go to A buffer (ph + 2) % 3 and B buffer ph % 2.
-  auto phase_step = [&](auto PH, int32_t t) __attribute__((always_inline)) {
+  auto phase_step = [&](auto PH, int32_t t, bool all_live) __attribute__((always_inline)) {
     constexpr int ph = decltype(PH)::value;
-    const StageSrc d = next_src(t + 2 < ksteps);
+    const StageSrc d = next_src(all_live || t + 2 < ksteps);
     if constexpr (ph % 2 == 0)
       step(smA[ph % 3], smA[(ph + 1) % 3], smB[(ph + 1) % 2], smA[(ph + 2) % 3], smB[ph % 2], d,
            F0, F1, F2, F3, S0, S1);
@@ -2181,11 +2204,21 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
       step(smA[ph % 3], smA[(ph + 1) % 3], smB[(ph + 1) % 2], smA[(ph + 2) % 3], smB[ph % 2], d,
            S0, S1, F2, F3, F0, F1);
   };
-  // One loop over groups of 6 steps, each behind a (uniform) bound check, so
-  // that no loop state outlives the loop.
+  // Groups of 6 steps whose loads (stages up to t + 7) all exist, then the
+  // remaining steps (at most 7) in groups of 6 with each step behind a
+  // (uniform) bound check.
+  int32_t t = 0;
+  for (; t + 8 <= ksteps; t += 6) {
+    phase_step(std::integral_constant<int, 0>{}, t, true);
+    phase_step(std::integral_constant<int, 1>{}, t + 1, true);
+    phase_step(std::integral_constant<int, 2>{}, t + 2, true);
+    phase_step(std::integral_constant<int, 3>{}, t + 3, true);
+    phase_step(std::integral_constant<int, 4>{}, t + 4, true);
+    phase_step(std::integral_constant<int, 5>{}, t + 5, true);
+  }
 #define CCL_FP8P_PHASE(k) \
-  if (t + k < ksteps) phase_step(std::integral_constant<int, k>{}, t + k)
-  for (int32_t t = 0; t < ksteps; t += 6) {
+  if (t + k < ksteps) phase_step(std::integral_constant<int, k>{}, t + k, false)
+  for (; t < ksteps; t += 6) {
     CCL_FP8P_PHASE(0); CCL_FP8P_PHASE(1); CCL_FP8P_PHASE(2);
     CCL_FP8P_PHASE(3); CCL_FP8P_PHASE(4); CCL_FP8P_PHASE(5);
   }
@@ -2330,7 +2363,12 @@ hipError_t launch_gemm(const Plan& p, const void* A, const void* B, void* C,
       a.kslice % kBK8x == 0 && b.kslice % kBK8x == 0) {
     gp.ksteps = (int32_t)(p.K / kBK8x);
     gp.ksteps_per_split = gp.ksteps;
-    if (g.fp8_pipe) {
+    // the pipelined kernel's descriptors span the tile's rows of A and
+    // columns of B over all K blocks
+    const int64_t lim = ((int64_t)1 << 31) - 4096;
+    const bool fits = (p.K / a.kslice - 1) * a.slice + 256 * (int64_t)a.ld < lim &&
+                      (p.K / b.kslice - 1) * b.slice + (int64_t)b.kslice * b.ld + 256 < lim;
+    if (g.fp8_pipe && fits) {
       hipLaunchKernelGGL(gemm_fp8p_kernel, grid, dim3(TileFp8P::THREADS), 0, stream, gp);
       return hipGetLastError();
     }

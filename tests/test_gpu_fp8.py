@@ -201,15 +201,16 @@ def _run_pipe(on, A, B, M, N, K, G, Gr, c_type):
     return cbuf, grid
 
 
-@pytest.mark.parametrize("M,N,K,G,Gr", [(512, 512, 128 * s, 1, 1) for s in (1, 2, 3, 4, 5, 6, 7, 8, 11, 13)]
+@pytest.mark.parametrize("M,N,K,G,Gr", [(512, 512, 128 * s, 1, 1)
+                                        for s in (1, 2, 3, 4, 5, 6, 7, 8, 11, 13, 14, 19, 20)]
                          + [(2048, 2048, 1024, 8, 2), (2048, 2048, 2048, 8, 1), (2048, 2048, 2048, 8, 8)])
 @pytest.mark.parametrize("c_type", [ccl.CCL_DT_BF16, ccl.CCL_DT_FP32])
 def test_fp8_pipelined_equals_two_stage_bit_for_bit(M, N, K, G, Gr, c_type):
     """The pipelined 16x16x128 kernel issues every accumulator's MFMAs in the
     same K order as the two-stage one, so C is identical bit for bit: for
-    step counts that stop inside the prologue, the first group of six steps
-    and later ones, and over CCL K blocks of 2 and 4 steps; and within the
-    oracle's tolerance."""
+    step counts that stop inside the prologue, the tail alone (up to 7
+    steps), one or more groups of six steps with tails of 0 to 7, and over
+    CCL K blocks of 2 and 4 steps; and within the oracle's tolerance."""
     A = W.draw_array_fp8(8700 + K + Gr, M, K, "normal", 1.0)
     B = W.draw_array_fp8(8800 + K + Gr, K, N, "normal", 1.0)
     on, (gr, gc) = _run_pipe(True, A, B, M, N, K, G, Gr, c_type)
