@@ -2226,11 +2226,16 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
 
   static_assert((BM / 2) * BN * 2 <= T::NSA * T::A_BYTES && (BM / 2) * BN * 2 <= T::NSB * T::B_BYTES,
                 "each half of the bf16 C tile fits in one operand's stage buffers");
+  // The lane index, made opaque here so that the epilogue's addresses are
+  // computed after the K loop instead of being hoisted before it (where
+  // they would stay live through the loop and spill).
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
   if (p.epi == 0 && !p.c_f32 && !p.ws)
     store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
-                                                                 pc, ti, tj, wm, wn, wave, lane);
+                                                                 pc, ti, tj, wm, wn, wave, ln);
   else
-    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, lane);
+    store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, ln);
 #endif
 }
 
