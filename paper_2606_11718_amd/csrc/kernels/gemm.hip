@@ -364,8 +364,8 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc (&acc)
 // in distinct banks. Then every wave copies BM / NW whole rows to C, 16
 // bytes per lane. NT marks the stores to C non-temporal (C is not read back
 // by the kernel); the 64-K-stage kernel uses it, where its Qwen3-shaped
-// launches (gate/up, dH) ran 1.5-3 % faster with it, measured alternating;
-// on the 256x256 kernels it made no measurable difference.
+// launches (gate/up, dH) ran 1.5-3 % faster with it, measured alternating,
+// and so does the pipelined fp8 kernel.
 template <int BM, int BN, int NW, int TM, int TN, int WM, int WN, bool NT = false>
 __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const f32x4 (&acc)[TM][TN],
                                                   char* lo, char* hi, int32_t pr, int32_t pc,
@@ -2238,9 +2238,11 @@ __global__ void __launch_bounds__(512, 2) gemm_fp8p_kernel(GemmParams p) {
   // they would stay live through the loop and spill).
   int ln = lane;
   asm volatile("" : "+v"(ln));
+  // Non-temporal C stores: at the power limit the fp8 GEMMs ran 1-4 % faster
+  // with them, at a 1 % higher clock (same box, alternating).
   if (p.epi == 0 && !p.c_f32 && !p.ws)
-    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN>(p, acc, &smA[0][0], &smB[0][0], pr,
-                                                                 pc, ti, tj, wm, wn, wave, ln);
+    store_tile_staged<BM, BN, T::NW, T::TM, T::TN, T::WM, T::WN, true>(
+        p, acc, &smA[0][0], &smB[0][0], pr, pc, ti, tj, wm, wn, wave, ln);
   else
     store_tile<BM, BN, 16, T::TM, T::TN, T::WM, T::WN>(p, acc, pr, pc, ti, tj, split, wm, wn, ln);
 #endif
